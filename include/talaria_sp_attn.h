@@ -1,0 +1,186 @@
+/*
+ * talaria_sp_attn -- session-prefill (SP) attention over a paged KV pool on
+ * one AMD Instinct MI355X (gfx950).
+ *
+ * The operation.  SP admission (paper Section 3.3, cold-pool scheduling)
+ * batch-prefills continuations of agent sessions whose prefix KV is already
+ * resident on the device; only the new tail is computed (Section 4.3, Host KV
+ * Registry: restore the agreed prefix into device slots, recompute only the
+ * unconfirmed tail).  For one attention layer and a batch of B sequences,
+ * sequence b has P_b cached tokens (its committed KV length, Section 4.1)
+ * and S_b new tokens.  New token i of sequence b sits at absolute position
+ * P_b + i and attends causally to keys 0 .. P_b + i:
+ *
+ *     o[b,i,h] = sum_j softmax_j( sigma * <q[b,i,h], k[b,j,g]> ) v[b,j,g],
+ *     lse[b,i,h] = ln sum_j exp( sigma * <q[b,i,h], k[b,j,g]> ),
+ *
+ * with g = h / (Hq / Hkv) (grouped-query attention) and sigma the softmax
+ * scale (default 1/sqrt(head_dim)).  Keys j < P_b come from the cached
+ * prefix; keys P_b .. P_b + S_b - 1 are the new tokens, which
+ * talaria_sp_attn_append_kv first writes into their pool slots.
+ *
+ * Memory.  The caller owns every buffer (pools, block tables, inputs,
+ * outputs, workspace); the library never allocates, frees or moves device
+ * memory and keeps no pointer across calls, so pool pages keep stable
+ * addresses (the stable-HBM-layout contract of Section 4.2).  Pages are
+ * allocated by the caller: block_tables[b][p] names the physical page that
+ * holds logical tokens p*page_size .. (p+1)*page_size - 1 of sequence b.
+ *
+ * Layouts (all bf16 tensors are raw 16-bit bfloat16, row-major):
+ *   q, out      [T][Hq][head_dim]             T = sum_b S_b, sequences in order
+ *   k_new,v_new [T][Hkv][head_dim]
+ *   lse         [T][Hq] float32 (natural log)
+ *   k_pool      [num_pages][Hkv][page_size][head_dim]
+ *   v_pool      [num_pages][Hkv][head_dim][page_size]   (token index innermost)
+ *   block_tables[num_seqs][max_pages_per_seq] int32 (device memory)
+ * One pool pair holds one layer ("layer-first" device layout, Appendix C).
+ * V pages keep tokens innermost so that the PV contraction, which reduces
+ * over tokens, reads its operands contiguously.
+ *
+ * Ordering.  Every call that takes a stream only enqueues work on it and
+ * returns; nothing synchronises.  For one batch: plan (host only), then
+ * append_kv, then prefill, on one stream (or with the caller's own
+ * ordering).  A plan is plain host data: it may be reused for any number of
+ * calls and copied freely.
+ *
+ * Errors.  Every call returns TALARIA_SP_OK (0) or a negative status and
+ * launches nothing on error; talaria_sp_last_error() then describes the
+ * failure (thread-local, valid until the next failing call on the thread).
+ * No C++ exception crosses this interface.
+ */
+#ifndef TALARIA_SP_ATTN_H
+#define TALARIA_SP_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TALARIA_SP_API __attribute__((visibility("default")))
+
+#define TALARIA_SP_OK 0
+#define TALARIA_SP_EINVAL (-1)       /* null pointer, negative length, bad geometry, short table */
+#define TALARIA_SP_EUNSUPPORTED (-2) /* head_dim, page_size, group size or batch size not built */
+#define TALARIA_SP_ENOSPACE (-3)     /* workspace smaller than the plan needs */
+#define TALARIA_SP_EHIP (-4)         /* the HIP runtime rejected a launch */
+
+/* Largest batch one plan describes (the plan travels as a kernel argument). */
+#define TALARIA_SP_MAX_SEQS 128
+/* Size of the opaque plan storage in 64-bit words. */
+#define TALARIA_SP_PLAN_WORDS 448
+
+/* Attention geometry of one layer's pool (the slab shape, page size and
+ * dtype of the KV layout descriptor, Appendix C).  Supported: head_dim 64
+ * or 128; page_size a power of two in [8, 256]; num_q_heads a multiple of
+ * num_kv_heads with num_q_heads / num_kv_heads <= 256. */
+typedef struct {
+    int32_t num_q_heads;
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t page_size;
+    int32_t num_pages;
+} talaria_sp_geom;
+
+/* Caller-owned plan storage, filled by talaria_sp_attn_plan. */
+typedef struct {
+    uint64_t opaque[TALARIA_SP_PLAN_WORDS];
+} talaria_sp_plan;
+
+/*
+ * Plan one SP batch (host only; touches no device state).
+ *
+ * geom                 pool geometry (host pointer).
+ * num_seqs             sequences in the batch, 0 .. TALARIA_SP_MAX_SEQS.
+ * prefix_lens          host int32[num_seqs]: cached tokens P_b >= 0.
+ * suffix_lens          host int32[num_seqs]: new tokens S_b >= 0 (0 = no-op).
+ * max_pages_per_seq    row stride of block_tables; must be at least
+ *                      ceil((P_b + S_b) / page_size) for every b.
+ * kv_splits            0 lets the planner split long key ranges across
+ *                      compute units; k > 0 forces exactly min(k, tiles)
+ *                      splits per query tile (tests use this).
+ * workspace_bytes      out: device workspace talaria_sp_attn_prefill needs
+ *                      (may be 0).
+ * plan                 out: the plan.
+ *
+ * The planner cuts every (sequence, KV head) into query tiles and splits
+ * each tile's visible key range into near-equal pieces, so a ragged batch
+ * spreads over all compute units; split results are merged by a
+ * log-sum-exp combine inside talaria_sp_attn_prefill.
+ */
+TALARIA_SP_API int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seqs,
+                         const int32_t* prefix_lens, const int32_t* suffix_lens,
+                         int32_t max_pages_per_seq, int32_t kv_splits,
+                         size_t* workspace_bytes, talaria_sp_plan* plan);
+
+/*
+ * Append: write the K and V rows of every new token into its pool slot
+ * (Section 4.3: the returning request's new tail goes into newly allocated
+ * device slots).  Token i of sequence b (row off_b + i of k_new / v_new)
+ * goes to logical position P_b + i, i.e. page
+ * block_tables[b][(P_b+i) / page_size], slot (P_b+i) mod page_size.  The
+ * copy is bit-exact; no other pool slot is written.  The caller guarantees
+ * that the pages named for positions P_b .. P_b+S_b-1 are distinct across
+ * the batch and below num_pages.
+ *
+ * k_new, v_new   device bf16 [T][Hkv][head_dim]
+ * k_pool, v_pool device bf16 pools (layouts above), written in place
+ * block_tables   device int32 [num_seqs][max_pages_per_seq]
+ * stream         hipStream_t (NULL = default stream)
+ */
+TALARIA_SP_API int talaria_sp_attn_append_kv(const talaria_sp_plan* plan, const void* k_new, const void* v_new,
+                              void* k_pool, void* v_pool, const int32_t* block_tables,
+                              void* stream);
+
+/*
+ * Prefill: causal attention of every new token over its sequence's cached
+ * prefix plus the new tokens (the batched prefill T_pf of an SP step,
+ * Section 3.3), reading K/V through the block tables.  append_kv for the
+ * same plan must have been enqueued first.  Pool slots past P_b + S_b in a
+ * sequence's last page, and block-table entries past its last page, are
+ * never read, so stale contents there (even NaN) do not matter.
+ *
+ * q              device bf16 [T][Hq][head_dim] (positional encoding applied)
+ * k_pool, v_pool device bf16 pools holding positions 0 .. P_b+S_b-1
+ * block_tables   device int32 [num_seqs][max_pages_per_seq]
+ * sm_scale       softmax scale sigma; <= 0 selects 1/sqrt(head_dim)
+ * out            device bf16 [T][Hq][head_dim] (round to nearest even)
+ * lse            device float32 [T][Hq] or NULL
+ * workspace      device buffer of at least workspace_bytes from the plan
+ *                (NULL allowed when that is 0); contents are scratch
+ * stream         hipStream_t (NULL = default stream)
+ *
+ * For a fixed plan the result is bitwise deterministic.
+ */
+TALARIA_SP_API int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const void* q, const void* k_pool,
+                            const void* v_pool, const int32_t* block_tables, float sm_scale,
+                            void* out, float* lse, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/*
+ * Gather: copy positions 0 .. P_b+S_b-1 of every sequence out of the pool
+ * into contiguous token-major rows -- the block-table page walk that the
+ * prefill kernel performs internally, as a standalone copy (the layer-first
+ * page view of Appendix C turned into a flat per-sequence view).
+ *
+ * k_out, v_out   device bf16 [sum_b (P_b+S_b)][Hkv][head_dim], sequences in order
+ */
+TALARIA_SP_API int talaria_sp_attn_gather_kv(const talaria_sp_plan* plan, const void* k_pool,
+                              const void* v_pool, const int32_t* block_tables, void* k_out,
+                              void* v_out, void* stream);
+
+/* Introspection of a plan's work list (host only).  Writes up to max_items
+ * records of 8 int32 each: {sequence, kv_head, first_token, num_tokens,
+ * key_begin, key_end, split, num_splits}; keys are absolute positions.
+ * Returns the number of work items (>= 0) or a negative status. */
+TALARIA_SP_API int talaria_sp_attn_plan_items(const talaria_sp_plan* plan, int32_t* items, int32_t max_items);
+
+/* Message for the last failing call on this thread ("" if none). */
+TALARIA_SP_API const char* talaria_sp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TALARIA_SP_ATTN_H */

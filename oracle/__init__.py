@@ -30,8 +30,8 @@ def _load(path: Optional[str] = None):
         lib = ctypes.CDLL(path)
         p = ctypes.c_void_p
         i32, i64, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
-        lib.oracle_append_kv.argtypes = [i32, p, p, p, i64, i32, i64, i64, p, p, p, p]
-        lib.oracle_gather_kv.argtypes = [i32, p, p, p, i64, i32, i64, i64, p, p, p, p]
+        lib.oracle_append_kv.argtypes = [i32, p, p, p, i64, i32, i64, i32, i32, p, p, p, p]
+        lib.oracle_gather_kv.argtypes = [i32, p, p, p, i64, i32, i64, i32, i32, p, p, p, p]
         lib.oracle_sp_attention.argtypes = [i32, p, p, p, i64, i32, i64, i32, i32, i32, f64,
                                             p, p, p, i64, p, p, p]
         lib.oracle_attention_contiguous.argtypes = [i32, p, p, i32, i32, i32, f64, p, p, p,
@@ -68,9 +68,9 @@ def append_kv(prefix_lens, suffix_lens, block_tables, page_size: int,
     pre, suf, bt = _i32(prefix_lens), _i32(suffix_lens), _i32(block_tables)
     kp, vp = np.array(k_pool, dtype=np.uint16, copy=True), np.array(v_pool, dtype=np.uint16, copy=True)
     kn, vn = _u16(k_new), _u16(v_new)
-    row_elems = int(np.prod(kp.shape[2:]))
+    Hkv, d = kp.shape[1], kp.shape[3]
     rc = _load(lib_path).oracle_append_kv(pre.shape[0], _ptr(pre), _ptr(suf), _ptr(bt), bt.shape[1],
-                                  page_size, kp.shape[0], row_elems, _ptr(kn), _ptr(vn),
+                                  page_size, kp.shape[0], Hkv, d, _ptr(kn), _ptr(vn),
                                   _ptr(kp), _ptr(vp))
     if rc != 0:
         raise ValueError(f"oracle_append_kv failed ({rc})")
@@ -84,11 +84,11 @@ def gather_kv(prefix_lens, suffix_lens, block_tables, page_size: int,
     pre, suf, bt = _i32(prefix_lens), _i32(suffix_lens), _i32(block_tables)
     kp, vp = _u16(k_pool), _u16(v_pool)
     n = int(pre.astype(np.int64).sum() + suf.astype(np.int64).sum())
-    ko = np.empty((n,) + kp.shape[2:], dtype=np.uint16)
+    Hkv, d = kp.shape[1], kp.shape[3]
+    ko = np.empty((n, Hkv, d), dtype=np.uint16)
     vo = np.empty_like(ko)
-    row_elems = int(np.prod(kp.shape[2:]))
     rc = _load(lib_path).oracle_gather_kv(pre.shape[0], _ptr(pre), _ptr(suf), _ptr(bt), bt.shape[1],
-                                  page_size, kp.shape[0], row_elems, _ptr(kp), _ptr(vp),
+                                  page_size, kp.shape[0], Hkv, d, _ptr(kp), _ptr(vp),
                                   _ptr(ko), _ptr(vo))
     if rc != 0:
         raise ValueError(f"oracle_gather_kv failed ({rc})")
@@ -101,14 +101,15 @@ def sp_attention(prefix_lens, suffix_lens, block_tables, page_size: int, q: np.n
                  lib_path: Optional[str] = None) -> Tuple[np.ndarray, np.ndarray]:
     """fp64 SP attention through block tables.
 
-    ``q`` is [T, Hq, d] bf16 bits; pools are [num_pages, page_size, Hkv, d].
+    ``q`` is [T, Hq, d] bf16 bits; the K pool is [num_pages, Hkv, page_size, d]
+    and the V pool [num_pages, Hkv, d, page_size].
     Returns (o [R, d], lse [R]) for the flat rows ``rows`` (token * Hq + head),
     or (o [T, Hq, d], lse [T, Hq]) when ``rows`` is None.
     """
     pre, suf, bt = _i32(prefix_lens), _i32(suffix_lens), _i32(block_tables)
     qb, kp, vp = _u16(q), _u16(k_pool), _u16(v_pool)
     T, Hq, d = qb.shape
-    Hkv = kp.shape[2]
+    Hkv = kp.shape[1]
     if rows is None:
         o = np.empty((T * Hq, d), dtype=np.float64)
         lse = np.empty(T * Hq, dtype=np.float64)

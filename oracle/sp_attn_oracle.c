@@ -20,7 +20,10 @@
  *   Logical position t of sequence b is stored in the page pool at page
  *   block_tables[b][t / page_size], slot t mod page_size (the paged device
  *   KV layout that HKVR restores into, Appendix C, "layer-first" view:
- *   one layer's pool, pages within the layer).
+ *   one layer's pool, pages within the layer).  Within a page the K pool is
+ *   [Hkv][page_size][d] and the V pool [Hkv][d][page_size]:
+ *       K(t, g, e) = k_pool[((page * Hkv + g) * page_size + slot) * d + e]
+ *       V(t, g, e) = v_pool[((page * Hkv + g) * d + e) * page_size + slot]
  *
  * Precision: inputs are bf16 bit patterns widened exactly to double; every
  * product, sum, exp and log is double.  Softmax is two-pass (max, then
@@ -65,15 +68,28 @@ static int64_t slot_of(const int32_t *block_tables, int64_t bt_stride, int64_t b
     return page * page_size + t % page_size;
 }
 
+/* Flat offsets of element (g, e) of pool slot (page, slot). */
+static int64_t k_index(int64_t page, int64_t slot, int64_t g, int64_t e, int64_t Hkv,
+                       int64_t page_size, int64_t d)
+{
+    return ((page * Hkv + g) * page_size + slot) * d + e;
+}
+
+static int64_t v_index(int64_t page, int64_t slot, int64_t g, int64_t e, int64_t Hkv,
+                       int64_t page_size, int64_t d)
+{
+    return ((page * Hkv + g) * d + e) * page_size + slot;
+}
+
 /*
  * Append: copy the K and V rows of every new token into its pool slot.
  * The new tokens of sequence b are rows off_b .. off_b + S_b - 1 of k_new /
- * v_new ([T][row_elems]); token i goes to logical position P_b + i.  Every
+ * v_new ([T][Hkv][d]); token i goes to logical position P_b + i.  Every
  * other pool slot keeps its bits.
  */
 int oracle_append_kv(int32_t num_seqs, const int32_t *prefix_lens, const int32_t *suffix_lens,
                      const int32_t *block_tables, int64_t bt_stride, int32_t page_size,
-                     int64_t num_pages, int64_t row_elems,
+                     int64_t num_pages, int32_t Hkv, int32_t d,
                      const uint16_t *k_new, const uint16_t *v_new,
                      uint16_t *k_pool, uint16_t *v_pool)
 {
@@ -83,13 +99,16 @@ int oracle_append_kv(int32_t num_seqs, const int32_t *prefix_lens, const int32_t
             int64_t t = (int64_t)prefix_lens[b] + i;
             if (t / page_size >= bt_stride)
                 return -1;
-            int64_t slot = slot_of(block_tables, bt_stride, b, t, page_size, num_pages);
-            if (slot < 0)
+            int64_t flat = slot_of(block_tables, bt_stride, b, t, page_size, num_pages);
+            if (flat < 0)
                 return -1;
-            for (int64_t e = 0; e < row_elems; ++e) {
-                k_pool[slot * row_elems + e] = k_new[(off + i) * row_elems + e];
-                v_pool[slot * row_elems + e] = v_new[(off + i) * row_elems + e];
-            }
+            int64_t page = flat / page_size, slot = flat % page_size;
+            for (int64_t g = 0; g < Hkv; ++g)
+                for (int64_t e = 0; e < d; ++e) {
+                    int64_t src = ((off + i) * Hkv + g) * d + e;
+                    k_pool[k_index(page, slot, g, e, Hkv, page_size, d)] = k_new[src];
+                    v_pool[v_index(page, slot, g, e, Hkv, page_size, d)] = v_new[src];
+                }
         }
         off += suffix_lens[b];
     }
@@ -98,11 +117,12 @@ int oracle_append_kv(int32_t num_seqs, const int32_t *prefix_lens, const int32_t
 
 /*
  * Gather: copy every logical token 0 .. P_b + S_b - 1 of every sequence
- * from the pool into contiguous rows (sequence-major), bit for bit.
+ * from the pool into contiguous rows [sum(P+S)][Hkv][d] (sequence-major),
+ * bit for bit.
  */
 int oracle_gather_kv(int32_t num_seqs, const int32_t *prefix_lens, const int32_t *suffix_lens,
                      const int32_t *block_tables, int64_t bt_stride, int32_t page_size,
-                     int64_t num_pages, int64_t row_elems,
+                     int64_t num_pages, int32_t Hkv, int32_t d,
                      const uint16_t *k_pool, const uint16_t *v_pool,
                      uint16_t *k_out, uint16_t *v_out)
 {
@@ -112,13 +132,16 @@ int oracle_gather_kv(int32_t num_seqs, const int32_t *prefix_lens, const int32_t
         for (int64_t t = 0; t < n; ++t) {
             if (t / page_size >= bt_stride)
                 return -1;
-            int64_t slot = slot_of(block_tables, bt_stride, b, t, page_size, num_pages);
-            if (slot < 0)
+            int64_t flat = slot_of(block_tables, bt_stride, b, t, page_size, num_pages);
+            if (flat < 0)
                 return -1;
-            memcpy(k_out + (off + t) * row_elems, k_pool + slot * row_elems,
-                   (size_t)row_elems * sizeof(uint16_t));
-            memcpy(v_out + (off + t) * row_elems, v_pool + slot * row_elems,
-                   (size_t)row_elems * sizeof(uint16_t));
+            int64_t page = flat / page_size, slot = flat % page_size;
+            for (int64_t g = 0; g < Hkv; ++g)
+                for (int64_t e = 0; e < d; ++e) {
+                    int64_t dst = ((off + t) * Hkv + g) * d + e;
+                    k_out[dst] = k_pool[k_index(page, slot, g, e, Hkv, page_size, d)];
+                    v_out[dst] = v_pool[v_index(page, slot, g, e, Hkv, page_size, d)];
+                }
         }
         off += n;
     }
@@ -160,8 +183,8 @@ static void attend_row(const double *qrow, const double *K, const double *V, int
  * rows == NULL means every row r = token * Hq + h in order; otherwise rows
  * lists num_rows flat row ids and output k belongs to rows[k].
  */
-typedef int (*fetch_fn)(const void *ctx, int32_t b, int64_t t, int32_t g,
-                        const uint16_t **krow, const uint16_t **vrow);
+typedef int (*fetch_fn)(const void *ctx, int32_t b, int64_t t, int32_t g, uint16_t *krow,
+                        uint16_t *vrow);
 
 static int attention_driver(int32_t num_seqs, const int32_t *prefix_lens,
                             const int32_t *suffix_lens, int32_t Hq, int32_t Hkv, int32_t d,
@@ -197,10 +220,11 @@ static int attention_driver(int32_t num_seqs, const int32_t *prefix_lens,
             status = -3;
             break;
         }
-        for (int32_t g = 0; g < Hkv && status == 0; ++g) {
+        uint16_t *kr = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)d);
+        uint16_t *vr = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)d);
+        for (int32_t g = 0; g < Hkv && status == 0 && kr && vr; ++g) {
             for (int64_t t = 0; t < n; ++t) {
-                const uint16_t *kr, *vr;
-                if (fetch(ctx, b, t, g, &kr, &vr) != 0) {
+                if (fetch(ctx, b, t, g, kr, vr) != 0) {
                     status = -1;
                     break;
                 }
@@ -232,6 +256,10 @@ static int attention_driver(int32_t num_seqs, const int32_t *prefix_lens,
                 free(qrow);
             }
         }
+        if (!kr || !vr)
+            status = -3;
+        free(kr);
+        free(vr);
         free(K);
         free(V);
     }
@@ -250,24 +278,26 @@ struct paged_ctx {
     const uint16_t *v_pool;
 };
 
-static int fetch_paged(const void *vctx, int32_t b, int64_t t, int32_t g,
-                       const uint16_t **krow, const uint16_t **vrow)
+static int fetch_paged(const void *vctx, int32_t b, int64_t t, int32_t g, uint16_t *krow,
+                       uint16_t *vrow)
 {
     const struct paged_ctx *c = (const struct paged_ctx *)vctx;
     if (t / c->page_size >= c->bt_stride)
         return -1;
-    int64_t slot = slot_of(c->block_tables, c->bt_stride, b, t, c->page_size, c->num_pages);
-    if (slot < 0)
+    int64_t flat = slot_of(c->block_tables, c->bt_stride, b, t, c->page_size, c->num_pages);
+    if (flat < 0)
         return -1;
-    int64_t base = (slot * c->Hkv + g) * (int64_t)c->d;
-    *krow = c->k_pool + base;
-    *vrow = c->v_pool + base;
+    int64_t page = flat / c->page_size, slot = flat % c->page_size;
+    for (int64_t e = 0; e < c->d; ++e) {
+        krow[e] = c->k_pool[k_index(page, slot, g, e, c->Hkv, c->page_size, c->d)];
+        vrow[e] = c->v_pool[v_index(page, slot, g, e, c->Hkv, c->page_size, c->d)];
+    }
     return 0;
 }
 
 /*
- * SP attention reading K/V through block tables from the pools
- * k_pool/v_pool [num_pages][page_size][Hkv][d] (the pool must already hold
+ * SP attention reading K/V through block tables from the pools (layouts
+ * in the header comment; the pool must already hold
  * the new tokens' K/V, i.e. append has run).  q is [T][Hq][d]; o is
  * [rows][d] and lse [rows] (natural log).  sm_scale <= 0 selects 1/sqrt(d).
  */
@@ -293,13 +323,13 @@ struct contig_ctx {
     const uint16_t *v_all;
 };
 
-static int fetch_contig(const void *vctx, int32_t b, int64_t t, int32_t g,
-                        const uint16_t **krow, const uint16_t **vrow)
+static int fetch_contig(const void *vctx, int32_t b, int64_t t, int32_t g, uint16_t *krow,
+                        uint16_t *vrow)
 {
     const struct contig_ctx *c = (const struct contig_ctx *)vctx;
     int64_t base = ((c->kv_off[b] + t) * c->Hkv + g) * (int64_t)c->d;
-    *krow = c->k_all + base;
-    *vrow = c->v_all + base;
+    memcpy(krow, c->k_all + base, sizeof(uint16_t) * (size_t)c->d);
+    memcpy(vrow, c->v_all + base, sizeof(uint16_t) * (size_t)c->d);
     return 0;
 }
 

@@ -1,0 +1,245 @@
+"""Python binding of libtalaria_sp_attn (session-prefill attention on MI355X).
+
+Argument marshalling only: every step of the path (append, page gather,
+prefill, combine) runs in the HIP library.  There is no CPU fallback; if the
+library has not been built, every call raises.
+
+The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
+
+    sp = plan(geom, prefix_lens, suffix_lens, max_pages_per_seq)
+    append_kv(sp, k_new, v_new, k_pool, v_pool, block_tables)
+    prefill(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)
+
+Device arrays are ``torch`` tensors (bf16 data may also be passed as int16
+or uint16 bit patterns); torch provides device memory and the current
+stream, nothing else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtalaria_sp_attn.so")
+
+OK, EINVAL, EUNSUPPORTED, ENOSPACE, EHIP = 0, -1, -2, -3, -4
+MAX_SEQS = 128
+PLAN_WORDS = 448
+ITEM_FIELDS = ("seq", "kv_head", "first_token", "num_tokens", "key_begin", "key_end", "split",
+               "num_splits")
+
+
+class TalariaError(RuntimeError):
+    """A negative status from the library; ``.status`` holds the code."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"[{status}] {message}")
+        self.status = status
+
+
+class Geom(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32)]
+
+
+class _RawPlan(ctypes.Structure):
+    _fields_ = [("opaque", ctypes.c_uint64 * PLAN_WORDS)]
+
+
+_lib = None
+
+
+def library() -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -c 'import __graft_entry__ as g; g.build()'`")
+        lib = ctypes.CDLL(LIB_PATH)
+        p, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        lib.talaria_sp_attn_plan.argtypes = [ctypes.POINTER(Geom), i32, p, p, i32, i32,
+                                             ctypes.POINTER(sz), ctypes.POINTER(_RawPlan)]
+        lib.talaria_sp_attn_append_kv.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p]
+        lib.talaria_sp_attn_prefill.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
+                                                ctypes.c_float, p, p, p, sz, p]
+        lib.talaria_sp_attn_gather_kv.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p]
+        lib.talaria_sp_attn_plan_items.argtypes = [ctypes.POINTER(_RawPlan), p, i32]
+        for f in (lib.talaria_sp_attn_plan, lib.talaria_sp_attn_append_kv,
+                  lib.talaria_sp_attn_prefill, lib.talaria_sp_attn_gather_kv,
+                  lib.talaria_sp_attn_plan_items):
+            f.restype = ctypes.c_int
+        lib.talaria_sp_last_error.argtypes = []
+        lib.talaria_sp_last_error.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def last_error() -> str:
+    return library().talaria_sp_last_error().decode()
+
+
+def _check(status: int) -> int:
+    if status < 0:
+        raise TalariaError(status, last_error())
+    return status
+
+
+@dataclass
+class SpPlan:
+    """A plan plus the host-side facts the binding uses for shape checks."""
+
+    raw: _RawPlan
+    geom: Geom
+    prefix_lens: np.ndarray
+    suffix_lens: np.ndarray
+    max_pages_per_seq: int
+    workspace_bytes: int
+
+    @property
+    def total_tokens(self) -> int:
+        return int(self.suffix_lens.sum())
+
+    @property
+    def total_kv_tokens(self) -> int:
+        return int(self.prefix_lens.astype(np.int64).sum() + self.suffix_lens.sum())
+
+    @property
+    def num_seqs(self) -> int:
+        return int(self.prefix_lens.shape[0])
+
+
+def make_geom(num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int,
+              num_pages: int) -> Geom:
+    return Geom(num_q_heads, num_kv_heads, head_dim, page_size, num_pages)
+
+
+def plan(geom: Geom, prefix_lens: Sequence[int], suffix_lens: Sequence[int],
+         max_pages_per_seq: int, kv_splits: int = 0) -> SpPlan:
+    """talaria_sp_attn_plan (host only)."""
+    pre = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+    suf = np.ascontiguousarray(suffix_lens, dtype=np.int32)
+    if pre.shape != suf.shape or pre.ndim != 1:
+        raise ValueError("prefix_lens and suffix_lens must be 1-D with equal length")
+    raw = _RawPlan()
+    ws = ctypes.c_size_t(0)
+    _check(library().talaria_sp_attn_plan(ctypes.byref(geom), pre.shape[0],
+                                          pre.ctypes.data if pre.size else None,
+                                          suf.ctypes.data if suf.size else None,
+                                          int(max_pages_per_seq), int(kv_splits),
+                                          ctypes.byref(ws), ctypes.byref(raw)))
+    return SpPlan(raw, geom, pre.copy(), suf.copy(), int(max_pages_per_seq), int(ws.value))
+
+
+def plan_items(sp: SpPlan) -> np.ndarray:
+    """The plan's work list as int32 [num_items, 8] (fields in ITEM_FIELDS)."""
+    n = _check(library().talaria_sp_attn_plan_items(ctypes.byref(sp.raw), None, 0))
+    out = np.zeros((max(n, 1), 8), dtype=np.int32)
+    _check(library().talaria_sp_attn_plan_items(ctypes.byref(sp.raw), out.ctypes.data, n))
+    return out[:n]
+
+
+# ---- device-side calls --------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+_BF16_LIKE = None
+
+
+def _dev(t, shape, what: str, bits16: bool = True, dtype=None):
+    """Validate a device tensor and return its address."""
+    torch = _torch()
+    global _BF16_LIKE
+    if _BF16_LIKE is None:
+        _BF16_LIKE = {torch.bfloat16, torch.int16, torch.uint16}
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{what} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be on a GPU")
+    if bits16 and t.dtype not in _BF16_LIKE:
+        raise TypeError(f"{what} must be bf16 (or 16-bit bit patterns), got {t.dtype}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return _torch().cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _pool_shapes(sp: SpPlan):
+    g = sp.geom
+    k = (g.num_pages, g.num_kv_heads, g.page_size, g.head_dim)
+    v = (g.num_pages, g.num_kv_heads, g.head_dim, g.page_size)
+    return k, v
+
+
+def append_kv(sp: SpPlan, k_new, v_new, k_pool, v_pool, block_tables, stream=None) -> None:
+    """talaria_sp_attn_append_kv: scatter the new tokens' K/V into their pages."""
+    torch = _torch()
+    g = sp.geom
+    kshape, vshape = _pool_shapes(sp)
+    row = (sp.total_tokens, g.num_kv_heads, g.head_dim)
+    args = (_dev(k_new, row, "k_new"), _dev(v_new, row, "v_new"),
+            _dev(k_pool, kshape, "k_pool"), _dev(v_pool, vshape, "v_pool"),
+            _dev(block_tables, (sp.num_seqs, sp.max_pages_per_seq), "block_tables",
+                 bits16=False, dtype=torch.int32))
+    _check(library().talaria_sp_attn_append_kv(ctypes.byref(sp.raw), *args, _stream(stream)))
+
+
+def prefill(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspace=None,
+            sm_scale: float = 0.0, stream=None) -> None:
+    """talaria_sp_attn_prefill: causal SP attention into ``out`` (and ``lse``)."""
+    torch = _torch()
+    g = sp.geom
+    kshape, vshape = _pool_shapes(sp)
+    qshape = (sp.total_tokens, g.num_q_heads, g.head_dim)
+    lse_ptr = None
+    if lse is not None:
+        lse_ptr = _dev(lse, (sp.total_tokens, g.num_q_heads), "lse", bits16=False,
+                       dtype=torch.float32)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        if not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    args = (_dev(q, qshape, "q"), _dev(k_pool, kshape, "k_pool"), _dev(v_pool, vshape, "v_pool"),
+            _dev(block_tables, (sp.num_seqs, sp.max_pages_per_seq), "block_tables",
+                 bits16=False, dtype=torch.int32))
+    _check(library().talaria_sp_attn_prefill(ctypes.byref(sp.raw), *args, float(sm_scale),
+                                             _dev(out, qshape, "out"), lse_ptr, ws_ptr, ws_bytes,
+                                             _stream(stream)))
+
+
+def gather_kv(sp: SpPlan, k_pool, v_pool, block_tables, k_out, v_out, stream=None) -> None:
+    """talaria_sp_attn_gather_kv: pages -> contiguous token-major K/V rows."""
+    torch = _torch()
+    g = sp.geom
+    kshape, vshape = _pool_shapes(sp)
+    oshape = (sp.total_kv_tokens, g.num_kv_heads, g.head_dim)
+    _check(library().talaria_sp_attn_gather_kv(
+        ctypes.byref(sp.raw), _dev(k_pool, kshape, "k_pool"), _dev(v_pool, vshape, "v_pool"),
+        _dev(block_tables, (sp.num_seqs, sp.max_pages_per_seq), "block_tables", bits16=False,
+             dtype=torch.int32),
+        _dev(k_out, oshape, "k_out"), _dev(v_out, oshape, "v_out"), _stream(stream)))
+
+
+def workspace_tensor(sp: SpPlan, device="cuda"):
+    """A device byte buffer of the plan's workspace size (None if it needs none)."""
+    if sp.workspace_bytes == 0:
+        return None
+    return _torch().empty(sp.workspace_bytes, dtype=_torch().uint8, device=device)

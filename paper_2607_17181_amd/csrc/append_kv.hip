@@ -1,0 +1,119 @@
+// Append the new tokens' K/V into their pool pages (bit-exact copy).
+//
+// Section 4.3 of the paper: a returning session gets newly allocated device
+// slots and only its unconfirmed tail is recomputed; this kernel writes that
+// tail's K/V into the slots.  New token i of sequence b lands at logical
+// position P_b + i, i.e. page block_tables[b][(P_b+i) / page_size], slot
+// (P_b+i) mod page_size.  A suffix may start and end in the middle of a
+// page; slots outside [P_b, P_b + S_b) are never written.
+//
+// Work unit: one workgroup per (logical page touched by the suffix,
+// sequence, KV head).  K rows move as 16-byte chunks (page rows are
+// contiguous in both layouts).  V pages are stored tokens-innermost, so each
+// thread assembles 8 consecutive slots of one feature row and writes them
+// with one 16-byte store when the whole group lies inside the suffix.
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+namespace tsp {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(256) void append_kv_kernel(PlanData p, const uint16_t* __restrict__ k_new,
+                                                        const uint16_t* __restrict__ v_new,
+                                                        uint16_t* __restrict__ k_pool,
+                                                        uint16_t* __restrict__ v_pool,
+                                                        const int32_t* __restrict__ bt) {
+    const int b = blockIdx.y;
+    const int g = blockIdx.z;
+    const SeqDesc s = p.seq[b];
+    if (s.suffix_len == 0)
+        return;
+    const int ps = p.page_size;
+    const int lp = (s.prefix_len >> p.page_shift) + (int)blockIdx.x;
+    const int end = s.prefix_len + s.suffix_len;
+    if (lp * ps >= end)
+        return;
+    const int pos_lo = max(s.prefix_len, lp * ps);
+    const int pos_hi = min(end, (lp + 1) * ps);
+    const int64_t page = bt[(int64_t)b * p.bt_stride + lp];
+    const int hkv = p.num_kv_heads;
+
+    // K: token rows of D bf16 = D/8 chunks of 16 bytes.
+    constexpr int CH = D / 8;
+    const int ntok = pos_hi - pos_lo;
+    for (int c = threadIdx.x; c < ntok * CH; c += 256) {
+        const int pos = pos_lo + c / CH;
+        const int col = c % CH;
+        const int64_t row = s.tok_off + (pos - s.prefix_len);
+        const u32x4* src = reinterpret_cast<const u32x4*>(k_new + (row * hkv + g) * D) + col;
+        u32x4* dst = reinterpret_cast<u32x4*>(
+                         k_pool + ((page * hkv + g) * ps + (pos & (ps - 1))) * D) + col;
+        *dst = *src;
+    }
+
+    // V: page block [D][ps]; groups of 8 slots of one feature row.
+    const int slot_lo = pos_lo - lp * ps, slot_hi = pos_hi - lp * ps;
+    const int grp_lo = slot_lo >> 3, grp_hi = (slot_hi + 7) >> 3;
+    const int ngrp = grp_hi - grp_lo;
+    uint16_t* vpage = v_pool + (page * hkv + g) * (int64_t)D * ps;
+    const int64_t row0 = s.tok_off + (lp * ps - s.prefix_len);  // row of slot 0 (may be < tok_off)
+    for (int c = threadIdx.x; c < ngrp * D; c += 256) {
+        const int d = c / ngrp;
+        const int grp = grp_lo + c % ngrp;
+        const int s0 = grp * 8;
+        uint16_t* dst = vpage + (int64_t)d * ps + s0;
+        if (s0 >= slot_lo && s0 + 8 <= slot_hi) {
+            union {
+                u32x4 v;
+                uint16_t h[8];
+            } u;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                u.h[e] = v_new[((row0 + s0 + e) * hkv + g) * D + d];
+            *reinterpret_cast<u32x4*>(dst) = u.v;
+        } else {
+            for (int e = 0; e < 8; ++e) {
+                const int sl = s0 + e;
+                if (sl >= slot_lo && sl < slot_hi)
+                    dst[e] = v_new[((row0 + sl) * hkv + g) * D + d];
+            }
+        }
+    }
+}
+
+}  // namespace
+}  // namespace tsp
+
+using namespace tsp;
+
+extern "C" int talaria_sp_attn_append_kv(const talaria_sp_plan* plan, const void* k_new,
+                                         const void* v_new, void* k_pool, void* v_pool,
+                                         const int32_t* block_tables, void* stream) {
+    int status;
+    const PlanData* p = checked_plan(plan, &status);
+    if (!p)
+        return status;
+    if (p->total_tokens == 0)
+        return TALARIA_SP_OK;
+    if (!k_new || !v_new || !k_pool || !v_pool || !block_tables)
+        return fail(TALARIA_SP_EINVAL, "append_kv: k_new, v_new, k_pool, v_pool and "
+                    "block_tables must not be NULL");
+    dim3 grid(p->max_suffix_pages, p->num_seqs, p->num_kv_heads);
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    auto kn = static_cast<const uint16_t*>(k_new);
+    auto vn = static_cast<const uint16_t*>(v_new);
+    auto kp = static_cast<uint16_t*>(k_pool);
+    auto vp = static_cast<uint16_t*>(v_pool);
+    if (p->head_dim == 128)
+        hipLaunchKernelGGL(append_kv_kernel<128>, grid, dim3(256), 0, st, *p, kn, vn, kp, vp,
+                           block_tables);
+    else
+        hipLaunchKernelGGL(append_kv_kernel<64>, grid, dim3(256), 0, st, *p, kn, vn, kp, vp,
+                           block_tables);
+    return launch_status("append_kv");
+}

@@ -1,0 +1,21 @@
+// Host-side helpers shared by the C-ABI entry points: error reporting and
+// plan validation.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "plan_data.h"
+
+namespace tsp {
+
+// Record a failure for talaria_sp_last_error() and return `code`.
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+// Return the plan behind `plan` if it is a valid plan, else record EINVAL.
+const PlanData* checked_plan(const talaria_sp_plan* plan, int* status);
+
+// Map a HIP launch status to TALARIA_SP_OK / TALARIA_SP_EHIP.
+int launch_status(const char* what);
+
+}  // namespace tsp

@@ -1,0 +1,228 @@
+// Host planner for SP attention: argument validation, ragged offsets, and
+// the split of every query tile's key range into work items.
+//
+// The planner follows the shape of an SP step (Section 3.3): a bounded
+// batch of admitted continuations, each with its own committed prefix
+// length and new-token count.  It produces one flat work list that the
+// prefill kernel walks by block index:
+//
+//   sequence b  ->  query tiles of kRowsPerTile rows (tile_tokens tokens x
+//                   group query heads that share one KV head)
+//               ->  per KV head
+//               ->  num_splits near-equal ranges of the tile's visible keys
+//
+// The number of splits per sequence is chosen so that the whole batch fills
+// the GPU's 256 compute units with items of similar cost: long prefixes
+// are cut into more pieces, short ones are not cut at all.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace tsp {
+
+namespace {
+thread_local char g_error[512] = "";
+
+// Work items that run at once: one per compute unit of an MI355X.
+constexpr int kConcurrentItems = 256;
+// Never cut a key range below this many key tiles.
+constexpr int kMinTilesPerSplit = 8;
+}  // namespace
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+const PlanData* checked_plan(const talaria_sp_plan* plan, int* status) {
+    if (!plan) {
+        *status = fail(TALARIA_SP_EINVAL, "plan is NULL");
+        return nullptr;
+    }
+    const PlanData* p = reinterpret_cast<const PlanData*>(plan);
+    if (p->magic != kPlanMagic || p->version != kPlanVersion) {
+        *status = fail(TALARIA_SP_EINVAL, "plan was not produced by talaria_sp_attn_plan");
+        return nullptr;
+    }
+    *status = TALARIA_SP_OK;
+    return p;
+}
+
+int launch_status(const char* what) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return fail(TALARIA_SP_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
+    return TALARIA_SP_OK;
+}
+
+}  // namespace tsp
+
+using namespace tsp;
+
+extern "C" const char* talaria_sp_last_error(void) { return g_error; }
+
+extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seqs,
+                                    const int32_t* prefix_lens, const int32_t* suffix_lens,
+                                    int32_t max_pages_per_seq, int32_t kv_splits,
+                                    size_t* workspace_bytes, talaria_sp_plan* plan) {
+    if (!geom || !plan || !workspace_bytes)
+        return fail(TALARIA_SP_EINVAL, "geom, plan and workspace_bytes must not be NULL");
+    const int32_t hq = geom->num_q_heads, hkv = geom->num_kv_heads, d = geom->head_dim;
+    const int32_t ps = geom->page_size;
+    if (hq <= 0 || hkv <= 0 || hq % hkv != 0)
+        return fail(TALARIA_SP_EINVAL, "num_q_heads (%d) must be a positive multiple of "
+                    "num_kv_heads (%d)", hq, hkv);
+    if (geom->num_pages <= 0)
+        return fail(TALARIA_SP_EINVAL, "num_pages must be positive (got %d)", geom->num_pages);
+    if (d != 64 && d != 128)
+        return fail(TALARIA_SP_EUNSUPPORTED, "head_dim %d not supported (64 or 128)", d);
+    if (ps < 8 || ps > 256 || (ps & (ps - 1)) != 0)
+        return fail(TALARIA_SP_EUNSUPPORTED, "page_size %d not supported (power of two in "
+                    "[8, 256])", ps);
+    if (hq / hkv > kRowsPerTile)
+        return fail(TALARIA_SP_EUNSUPPORTED, "query group %d exceeds %d", hq / hkv, kRowsPerTile);
+    if (num_seqs < 0)
+        return fail(TALARIA_SP_EINVAL, "num_seqs must be >= 0 (got %d)", num_seqs);
+    if (num_seqs > TALARIA_SP_MAX_SEQS)
+        return fail(TALARIA_SP_EUNSUPPORTED, "num_seqs %d exceeds %d; split the batch",
+                    num_seqs, TALARIA_SP_MAX_SEQS);
+    if (num_seqs > 0 && (!prefix_lens || !suffix_lens))
+        return fail(TALARIA_SP_EINVAL, "prefix_lens and suffix_lens must not be NULL");
+    if (kv_splits < 0)
+        return fail(TALARIA_SP_EINVAL, "kv_splits must be >= 0 (got %d)", kv_splits);
+    if (max_pages_per_seq < 0)
+        return fail(TALARIA_SP_EINVAL, "max_pages_per_seq must be >= 0");
+
+    PlanData p;
+    memset(&p, 0, sizeof p);
+    p.magic = kPlanMagic;
+    p.version = kPlanVersion;
+    p.num_q_heads = hq;
+    p.num_kv_heads = hkv;
+    p.head_dim = d;
+    p.page_size = ps;
+    p.page_shift = __builtin_ctz((unsigned)ps);
+    p.num_pages = geom->num_pages;
+    p.num_seqs = num_seqs;
+    p.bt_stride = max_pages_per_seq;
+    p.group = hq / hkv;
+    p.tile_tokens = kRowsPerTile / p.group;
+
+    // Lengths, offsets and the cost of one unsplit item per sequence.
+    int64_t tok = 0, kvtok = 0;
+    int32_t tiles[TALARIA_SP_MAX_SEQS];
+    int32_t qtiles[TALARIA_SP_MAX_SEQS];
+    double total_cost = 0.0;
+    int64_t base_items = 0;
+    for (int32_t b = 0; b < num_seqs; ++b) {
+        const int64_t P = prefix_lens[b], S = suffix_lens[b];
+        if (P < 0 || S < 0)
+            return fail(TALARIA_SP_EINVAL, "sequence %d: negative length (P=%lld, S=%lld)", b,
+                        (long long)P, (long long)S);
+        if (P + S > INT32_MAX / 2)
+            return fail(TALARIA_SP_EINVAL, "sequence %d: P+S too large", b);
+        const int64_t pages = (P + S + ps - 1) / ps;
+        if (pages > max_pages_per_seq)
+            return fail(TALARIA_SP_EINVAL, "sequence %d needs %lld pages but the block-table "
+                        "stride is %d", b, (long long)pages, max_pages_per_seq);
+        p.seq[b].prefix_len = (int32_t)P;
+        p.seq[b].suffix_len = (int32_t)S;
+        p.seq[b].tok_off = (int32_t)tok;
+        p.kv_off[b] = (int32_t)kvtok;
+        tok += S;
+        kvtok += P + S;
+        if (tok > INT32_MAX / 2 || kvtok > INT32_MAX / 2)
+            return fail(TALARIA_SP_EINVAL, "batch too large");
+        qtiles[b] = (int32_t)((S + p.tile_tokens - 1) / p.tile_tokens);
+        tiles[b] = S > 0 ? (int32_t)((P + S + kKeysPerTile - 1) / kKeysPerTile) : 0;
+        base_items += (int64_t)qtiles[b] * hkv;
+        total_cost += (double)qtiles[b] * hkv * tiles[b];
+        if (S > 0) {
+            const int32_t first_page = (int32_t)(P / ps), last_page = (int32_t)((P + S - 1) / ps);
+            p.max_suffix_pages = std::max(p.max_suffix_pages, last_page - first_page + 1);
+        }
+        p.max_seq_pages = std::max(p.max_seq_pages, (int32_t)pages);
+    }
+    p.total_tokens = (int32_t)tok;
+    p.total_kv_tokens = (int32_t)kvtok;
+    p.kv_off[num_seqs] = (int32_t)kvtok;
+
+    // Target key tiles per item: the per-CU share of the batch when the
+    // batch alone cannot fill the GPU (one round of equal items), half of it
+    // otherwise (so that a long sequence's items cannot form a long tail).
+    double share = total_cost / kConcurrentItems;
+    if (base_items >= kConcurrentItems)
+        share *= 0.5;
+    const double target = std::max<double>(kMinTilesPerSplit, share);
+
+    int64_t items = 0, part_items = 0;
+    for (int32_t b = 0; b < num_seqs; ++b) {
+        int32_t nsp = 1;
+        if (tiles[b] > 0) {
+            if (kv_splits > 0)
+                nsp = kv_splits;
+            else
+                nsp = (int32_t)ceil(tiles[b] / target * 0.999);
+            nsp = std::max(1, std::min({nsp, tiles[b], kMaxSplits}));
+        }
+        p.seq[b].item_off = (int32_t)items;
+        p.seq[b].part_off = (int32_t)part_items;
+        const int64_t n = (int64_t)qtiles[b] * hkv * nsp;
+        items += n;
+        if (nsp > 1)
+            part_items += n;
+        if (items > INT32_MAX / 2)
+            return fail(TALARIA_SP_EINVAL, "too many work items");
+    }
+    p.seq[num_seqs].item_off = (int32_t)items;
+    p.seq[num_seqs].part_off = (int32_t)part_items;
+    p.seq[num_seqs].tok_off = (int32_t)tok;
+    p.num_items = (int32_t)items;
+    p.num_part_items = (int32_t)part_items;
+
+    const int64_t part_o = part_items * kRowsPerTile * (int64_t)d * 4;
+    const int64_t part_lse = part_items * kRowsPerTile * 4;
+    p.ws_lse_offset = (part_o + 255) & ~(int64_t)255;
+    p.ws_bytes = part_items ? p.ws_lse_offset + part_lse : 0;
+
+    memset(plan, 0, sizeof *plan);
+    memcpy(plan, &p, sizeof p);
+    *workspace_bytes = (size_t)p.ws_bytes;
+    return TALARIA_SP_OK;
+}
+
+extern "C" int talaria_sp_attn_plan_items(const talaria_sp_plan* plan, int32_t* items,
+                                          int32_t max_items) {
+    int status;
+    const PlanData* p = checked_plan(plan, &status);
+    if (!p)
+        return status;
+    if (max_items < 0 || (max_items > 0 && !items))
+        return fail(TALARIA_SP_EINVAL, "items must hold max_items records");
+    const int32_t n = std::min(max_items, p->num_items);
+    for (int32_t i = 0; i < n; ++i) {
+        const WorkItem w = decode_item(*p, i);
+        const int32_t P = p->seq[w.seq].prefix_len;
+        const int32_t kend_all = P + w.first_token + w.num_tokens;
+        int32_t* r = items + 8 * i;
+        r[0] = w.seq;
+        r[1] = w.kv_head;
+        r[2] = w.first_token;
+        r[3] = w.num_tokens;
+        r[4] = std::min(w.tile_begin * kKeysPerTile, kend_all);
+        r[5] = std::min(w.tile_end * kKeysPerTile, kend_all);
+        r[6] = w.split;
+        r[7] = w.num_splits;
+    }
+    return p->num_items;
+}

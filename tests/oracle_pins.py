@@ -248,17 +248,17 @@ def pin_append_scatter(lib=None):
     wl, kp, vp = _case(17, Hq=2, Hkv=2, d=8, ps=4, pre=(6, 0, 3), suf=(5, 9, 4), num_pages=30)
     kp2, vp2 = oracle.append_kv(wl.prefix_lens, wl.suffix_lens, wl.block_tables, wl.page_size,
                                 wl.k_new, wl.v_new, kp, vp, lib_path=lib)
-    ek = kp.reshape(-1, 2, 8).copy()
-    ev = vp.reshape(-1, 2, 8).copy()
+    ek = kp.copy()   # [page, Hkv, slot, d]
+    ev = vp.copy()   # [page, Hkv, d, slot]
     toff = 0
     for b in range(wl.num_seqs):
         P, S = int(wl.prefix_lens[b]), int(wl.suffix_lens[b])
         t = np.arange(P, P + S)
-        slots = wl.block_tables[b, t // 4].astype(np.int64) * 4 + t % 4
-        ek[slots] = wl.k_new[toff:toff + S]
-        ev[slots] = wl.v_new[toff:toff + S]
+        pages = wl.block_tables[b, t // 4]
+        ek[pages, :, t % 4, :] = wl.k_new[toff:toff + S]
+        ev[pages, :, :, t % 4] = wl.v_new[toff:toff + S]
         toff += S
-    assert np.array_equal(kp2.reshape(ek.shape), ek) and np.array_equal(vp2.reshape(ev.shape), ev)
+    assert np.array_equal(kp2, ek) and np.array_equal(vp2, ev)
 
 
 def pin_gather(lib=None):

@@ -1,0 +1,169 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its host planner covers every (query row, key) pair exactly once, balances
+work and rejects bad arguments without touching the device."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_17181_amd as tsa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "talaria_sp_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"TALARIA_SP_API\s+[\w\s\*]+?\b(talaria_\w+)\s*\(", text)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = tsa.library()
+    names = declared_functions()
+    assert len(names) == 6
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _geom(hq=8, hkv=1, d=128, ps=16, pages=100_000):
+    return tsa.make_geom(hq, hkv, d, ps, pages)
+
+
+def check_coverage(sp, geom):
+    """Every (seq, kv head, token) row sees keys 0..P+i exactly once."""
+    items = tsa.plan_items(sp)
+    tt = 256 // (geom.num_q_heads // geom.num_kv_heads)
+    seen = {}
+    for it in items:
+        b, g, ft, nt, kb, ke, s, ns = [int(x) for x in it]
+        key = (b, g, ft)
+        seen.setdefault(key, []).append((s, ns, kb, ke, nt))
+    for b in range(sp.num_seqs):
+        P, S = int(sp.prefix_lens[b]), int(sp.suffix_lens[b])
+        for g in range(geom.num_kv_heads):
+            covered_tokens = 0
+            for ft in range(0, S, tt):
+                parts = sorted(seen.pop((b, g, ft)))
+                nt = parts[0][4]
+                assert nt == min(tt, S - ft)
+                assert [p[0] for p in parts] == list(range(parts[0][1]))
+                # key ranges tile [0, P + ft + nt) in order, without overlap
+                pos = 0
+                for s, ns, kb, ke, _ in parts:
+                    assert kb == pos and ke >= kb
+                    pos = ke
+                assert pos == P + ft + nt
+                covered_tokens += nt
+            assert covered_tokens == S
+    assert not seen, "items for rows that do not exist"
+    return items
+
+
+@pytest.mark.parametrize("pre,suf", [([25_000], [2_048]), ([0, 0, 0, 0], [25_000] * 4),
+                                     ([256], [64]), ([105_000], [2_048]),
+                                     ([0, 7, 33_333, 129_000, 5], [1, 4096, 0, 517, 3000])])
+def test_plan_covers_every_pair_once(pre, suf):
+    geom = _geom(pages=1 << 30)
+    sp = tsa.plan(geom, pre, suf, max_pages_per_seq=(max(p + s for p, s in zip(pre, suf)) + 15) // 16)
+    check_coverage(sp, geom)
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(2, 1, 64), (8, 2, 128), (16, 16, 64), (12, 4, 128),
+                                      (32, 1, 128), (5, 5, 64)])
+@pytest.mark.parametrize("splits", [0, 1, 3, 64])
+def test_plan_covers_every_pair_once_geometries(hq, hkv, d, splits):
+    geom = _geom(hq, hkv, d, 16, 1 << 20)
+    rng = np.random.default_rng(hq * 100 + splits)
+    pre = rng.integers(0, 5000, size=5)
+    suf = rng.integers(0, 700, size=5)
+    sp = tsa.plan(geom, pre, suf, 500, kv_splits=splits)
+    items = check_coverage(sp, geom)
+    if splits:
+        assert (items[:, 7] <= splits).all()
+
+
+def test_single_continuation_fills_the_gpu_in_one_round():
+    geom = _geom()
+    sp = tsa.plan(geom, [25_000], [2_048], 1700)
+    items = tsa.plan_items(sp)
+    assert items.shape[0] == 256
+    keys = items[:, 5] - items[:, 4]
+    assert keys.max() - keys.min() <= 2 * 64 + 2048 // 4
+    # workspace: fp32 partial O + LSE for 256 rows of every split item
+    part = 256 * 256 * 128 * 4
+    assert sp.workspace_bytes == ((part + 255) // 256) * 256 + 256 * 256 * 4
+
+
+def test_unsplit_batch_needs_no_workspace():
+    sp = tsa.plan(_geom(), [0, 0, 0, 0], [25_000] * 4, 1600)
+    assert sp.workspace_bytes == 0
+    assert (tsa.plan_items(sp)[:, 7] == 1).all()
+
+
+def test_long_query_tiles_come_first():
+    sp = tsa.plan(_geom(), [0], [25_000], 1600)
+    items = tsa.plan_items(sp)
+    assert (np.diff(items[:, 2]) <= 0).all()
+
+
+@pytest.mark.parametrize("kwargs,code", [
+    (dict(geom=(8, 3, 128, 16, 10)), tsa.EINVAL),
+    (dict(geom=(8, 1, 96, 16, 10)), tsa.EUNSUPPORTED),
+    (dict(geom=(8, 1, 128, 12, 10)), tsa.EUNSUPPORTED),
+    (dict(geom=(8, 1, 128, 4, 10)), tsa.EUNSUPPORTED),
+    (dict(geom=(8, 1, 128, 16, 0)), tsa.EINVAL),
+    (dict(geom=(512, 1, 128, 16, 10)), tsa.EUNSUPPORTED),
+    (dict(pre=[-1]), tsa.EINVAL),
+    (dict(suf=[-5]), tsa.EINVAL),
+    (dict(stride=1), tsa.EINVAL),
+    (dict(splits=-1), tsa.EINVAL),
+    (dict(pre=[1] * 129, suf=[1] * 129), tsa.EUNSUPPORTED),
+])
+def test_plan_rejects_bad_arguments(kwargs, code):
+    g = tsa.make_geom(*kwargs.get("geom", (8, 1, 128, 16, 1000)))
+    pre = kwargs.get("pre", [20])
+    suf = kwargs.get("suf", [5])
+    with pytest.raises(tsa.TalariaError) as e:
+        tsa.plan(g, pre, suf, kwargs.get("stride", 4), kv_splits=kwargs.get("splits", 0))
+    assert e.value.status == code
+    assert tsa.last_error()
+
+
+def test_empty_batch_is_a_valid_plan():
+    sp = tsa.plan(_geom(), [], [], 0)
+    assert sp.workspace_bytes == 0 and tsa.plan_items(sp).shape[0] == 0
+    sp = tsa.plan(_geom(), [100, 50], [0, 0], 10)
+    assert tsa.plan_items(sp).shape[0] == 0
+
+
+def test_max_batch_accepted():
+    sp = tsa.plan(_geom(), [1000] * 128, [100] * 128, 70)
+    check_coverage(sp, _geom())
+
+
+def test_calls_reject_a_forged_plan():
+    raw = tsa._RawPlan()
+    lib = tsa.library()
+    st = lib.talaria_sp_attn_append_kv(raw, None, None, None, None, None, None)
+    assert st == tsa.EINVAL
+    st = lib.talaria_sp_attn_prefill(raw, None, None, None, None, 0.0, None, None, None, 0, None)
+    assert st == tsa.EINVAL
+    assert "talaria_sp_attn_plan" in tsa.last_error()
+
+
+def test_prefill_checks_arguments_before_launching():
+    sp = tsa.plan(_geom(), [25_000], [2_048], 1700)
+    lib = tsa.library()
+    # null pointers
+    st = lib.talaria_sp_attn_prefill(sp.raw, None, None, None, None, 0.0, None, None, None, 0,
+                                     None)
+    assert st == tsa.EINVAL
+    # workspace too small (dummy non-null addresses: nothing is launched on error)
+    fake = 4096
+    st = lib.talaria_sp_attn_prefill(sp.raw, fake, fake, fake, fake, 0.0, fake, None, fake, 16,
+                                     None)
+    assert st == tsa.ENOSPACE
+    st = lib.talaria_sp_attn_prefill(sp.raw, fake, fake, fake, fake, float("nan"), fake, None,
+                                     fake, sp.workspace_bytes, None)
+    assert st == tsa.EINVAL

@@ -24,12 +24,17 @@ MUTANTS = [
     ("no_normalisation", "o[e] /= l;", "o[e] /= 1.0;"),
     ("wrong_slot", "return page * page_size + t % page_size;",
      "return page * page_size + (page_size - 1 - t % page_size);"),
+    ("v_layout_untransposed", "return ((page * Hkv + g) * d + e) * page_size + slot;",
+     "return ((page * Hkv + g) * page_size + slot) * d + e;"),
     ("transposed_k", "dot += qrow[e] * K[j * d + e];", "dot += qrow[e] * K[e * n + j];"),
-    ("k_v_swapped", "*krow = c->k_pool + base;\n    *vrow = c->v_pool + base;",
-     "*krow = c->v_pool + base;\n    *vrow = c->k_pool + base;"),
-    ("append_ignores_seq_offset", "k_new[(off + i) * row_elems + e]", "k_new[i * row_elems + e]"),
+    ("k_v_swapped", "krow[e] = c->k_pool[k_index(page, slot, g, e, c->Hkv, c->page_size, c->d)];\n        vrow[e] = c->v_pool[v_index(page, slot, g, e, c->Hkv, c->page_size, c->d)];",
+     "krow[e] = c->v_pool[k_index(page, slot, g, e, c->Hkv, c->page_size, c->d)];\n        vrow[e] = c->k_pool[v_index(page, slot, g, e, c->Hkv, c->page_size, c->d)];"),
+    ("append_ignores_seq_offset", "int64_t src = ((off + i) * Hkv + g) * d + e;",
+     "int64_t src = (i * Hkv + g) * d + e;"),
     ("gather_misses_last_token", "int64_t n = (int64_t)prefix_lens[b] + suffix_lens[b];\n        for (int64_t t = 0; t < n; ++t) {\n            if",
      "int64_t n = (int64_t)prefix_lens[b] + suffix_lens[b];\n        for (int64_t t = 0; t + 1 < n; ++t) {\n            if"),
+    ("gather_head_mixup", "int64_t dst = ((off + t) * Hkv + g) * d + e;",
+     "int64_t dst = ((off + t) * Hkv + (Hkv - 1 - g)) * d + e;"),
     ("sign_flip_dot", "scores[j] = sigma * dot;", "scores[j] = -sigma * dot;"),
 ]
 

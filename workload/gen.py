@@ -128,17 +128,19 @@ class Workload:
         return 4 * self.head_dim * self.num_q_heads * self.visible_pairs()
 
     def pool_bits(self, fill: int = int(BF16_NAN)) -> Tuple[np.ndarray, np.ndarray]:
-        """Host K and V pools ``[num_pages, page_size, Hkv, d]`` with the prefix placed.
+        """Host K and V pools with the prefix placed; every other slot holds ``fill``.
 
-        Every slot that holds no prefix token holds ``fill``.
+        K pool ``[num_pages, Hkv, page_size, d]``; V pool
+        ``[num_pages, Hkv, d, page_size]`` (token index innermost).
         """
-        shape = (self.num_pages * self.page_size, self.num_kv_heads, self.head_dim)
-        kp = np.full(shape, fill, dtype=np.uint16)
-        vp = np.full(shape, fill, dtype=np.uint16)
-        kp[self.prefix_slots] = self.prefix_k
-        vp[self.prefix_slots] = self.prefix_v
-        final = (self.num_pages, self.page_size, self.num_kv_heads, self.head_dim)
-        return kp.reshape(final), vp.reshape(final)
+        P, H, ps, d = self.num_pages, self.num_kv_heads, self.page_size, self.head_dim
+        kp = np.full((P, H, ps, d), fill, dtype=np.uint16)
+        vp = np.full((P, H, d, ps), fill, dtype=np.uint16)
+        page = self.prefix_slots // ps
+        slot = self.prefix_slots % ps
+        kp[page, :, slot, :] = self.prefix_k
+        vp[page, :, :, slot] = self.prefix_v
+        return kp, vp
 
 
 def _draw_bits(rng: np.random.Generator, shape: Sequence[int], std: float) -> np.ndarray:

@@ -1,0 +1,267 @@
+#!/usr/bin/env python3
+"""Benchmark: session-prefill attention for one 25K-prefix continuation.
+
+One step = the whole hot path for one SP batch of one attention layer:
+plan (host) -> append_kv (new K/V into pool pages) -> prefill (paged causal
+attention; split key ranges merged by the LSE combine).  Inputs are seeded
+synthetic tensors already resident in HBM when timing starts.
+
+Workload: one continuation with a 25,000-token cached prefix and 2,048 new
+tokens, Hq=8 / Hkv=1 / head_dim=128 (one TP=8 rank's head share of a
+235B-class GQA model), page size 16, pages shuffled in a 100K-page pool.
+
+Prints ONE JSON line.  Extra figures (per-kernel times, other configs,
+standalone append/gather bandwidth) go to --extra-json when given.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+sys.path.insert(0, os.path.join(HERE, "tests"))
+
+METRIC = "SP prefill attention TFLOP/s (% bf16 MFMA peak); ms per 25K-prefix continuation"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="single",
+                    choices=["tiny", "single", "ragged", "long", "cold"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=16384,
+                    help="query rows of the workload the oracle baseline computes")
+    ap.add_argument("--extra-json", default=None,
+                    help="write per-kernel / per-config figures to this file")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="with --extra-json: also time every other config")
+    return ap.parse_args()
+
+
+def time_config(name, steps, warmup, torch, tsa, harness, workload):
+    """Time `steps` whole-path steps; return a dict of figures."""
+    wl = workload.make_workload(name)
+    db = harness.DeviceBatch(wl, fill=0)
+    flops = wl.flops()
+    n_chunks = len(wl.chunks)
+    stream = torch.cuda.current_stream()
+
+    # Plans are made inside the timed step (host work is part of the path);
+    # workspaces are allocated once up front, sized by a first plan.
+    plans0 = db.plans()
+    workspaces = [tsa.workspace_tensor(sp) for sp in plans0]
+    chunk_t = [db.chunk_tensors(c) for c in range(n_chunks)]
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * n_chunks + 1)]
+          for _ in range(steps)]
+    plan_s = 0.0
+
+    def step(events):
+        nonlocal plan_s
+        t0 = time.perf_counter()
+        plans = db.plans()
+        plan_s += time.perf_counter() - t0
+        if events is not None:
+            events[0].record(stream)
+        for c, sp in enumerate(plans):
+            q, kn, vn, out, lse, _ = chunk_t[c]
+            tsa.append_kv(sp, kn, vn, db.k_pool, db.v_pool, db.bt)
+            if events is not None:
+                events[2 * c + 1].record(stream)
+            tsa.prefill(sp, q, db.k_pool, db.v_pool, db.bt, out, lse, workspaces[c])
+            if events is not None:
+                events[2 * c + 2].record(stream)
+
+    for _ in range(warmup):
+        step(None)
+    torch.cuda.synchronize()
+    plan_s = 0.0
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    append_ms, prefill_ms = [], []
+    for e in ev:
+        a = p = 0.0
+        for c in range(n_chunks):
+            a += e[2 * c].elapsed_time(e[2 * c + 1])
+            p += e[2 * c + 1].elapsed_time(e[2 * c + 2])
+        append_ms.append(a)
+        prefill_ms.append(p)
+    ms_step = wall * 1e3 / steps
+    prefill_avg = float(np.mean(prefill_ms))
+    append_avg = float(np.mean(append_ms))
+    T = wl.total_tokens
+    append_bytes = 2 * 2 * T * wl.num_kv_heads * wl.head_dim * 2   # K+V, read + write
+    return {
+        "workload": name,
+        "flops": flops,
+        "ms_per_step": ms_step,
+        "tflops_step": flops / (ms_step * 1e-3) / 1e12,
+        "prefill_call_ms": prefill_avg,
+        "prefill_call_ms_p50": float(np.median(prefill_ms)),
+        "prefill_tflops": flops / (prefill_avg * 1e-3) / 1e12,
+        "append_ms": append_avg,
+        "append_gbs": append_bytes / (append_avg * 1e-3) / 1e9,
+        "plan_us": plan_s / steps * 1e6,
+        "num_items": [int(tsa.plan_items(sp).shape[0]) for sp in plans0],
+        "workspace_bytes": [sp.workspace_bytes for sp in plans0],
+        "wl": wl,
+        "db": db,
+    }
+
+
+def cpu_baseline(wl, rows_n, oracle, harness):
+    """The oracle timed on the host cores over a seeded sample of query rows."""
+    from workload import BF16_NAN
+    kp, vp = wl.pool_bits(fill=int(BF16_NAN))
+    kp, vp = oracle.append_kv(wl.prefix_lens, wl.suffix_lens, wl.block_tables, wl.page_size,
+                              wl.k_new, wl.v_new, kp, vp)
+    rng = np.random.default_rng(123)
+    rows_n = min(rows_n, wl.total_tokens * wl.num_q_heads)
+    rows = np.sort(rng.choice(wl.total_tokens * wl.num_q_heads, size=rows_n, replace=False))
+    # FLOPs of the sampled rows: 4 * d per visible (row, key) pair.
+    tok = rows // wl.num_q_heads
+    offs = np.concatenate([[0], np.cumsum(wl.suffix_lens)])
+    seq = np.searchsorted(offs, tok, side="right") - 1
+    visible = wl.prefix_lens[seq].astype(np.int64) + (tok - offs[seq]) + 1
+    flops = float(4 * wl.head_dim * visible.sum())
+    t0 = time.perf_counter()
+    oracle.sp_attention(wl.prefix_lens, wl.suffix_lens, wl.block_tables, wl.page_size, wl.q, kp,
+                        vp, rows=rows)
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{rows_n} of {wl.total_tokens * wl.num_q_heads} query rows (seeded) of "
+                      f"the same workload, fp64, {dt:.1f} s wall"}
+
+
+def standalone_bandwidth(torch, tsa, harness, workload, reps=20):
+    """Append and gather GB/s on inputs larger than the 256 MB Infinity Cache."""
+    res = {}
+    for name in ("cold", "ragged"):
+        wl = workload.make_workload(name)
+        db = harness.DeviceBatch(wl, fill=0)
+        sp = db.plans()[0]
+        # append
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt)
+        torch.cuda.synchronize()
+        t0.record()
+        for _ in range(reps):
+            tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / reps
+        nbytes = 2 * 2 * wl.total_tokens * wl.num_kv_heads * wl.head_dim * 2
+        res[f"append_{name}"] = {"ms": ms, "bytes": nbytes, "gbs": nbytes / ms / 1e6}
+        # gather
+        n = sp.total_kv_tokens
+        ko = torch.empty((n, wl.num_kv_heads, wl.head_dim), dtype=torch.int16, device="cuda")
+        vo = torch.empty_like(ko)
+        tsa.gather_kv(sp, db.k_pool, db.v_pool, db.bt, ko, vo)
+        torch.cuda.synchronize()
+        t0.record()
+        for _ in range(reps):
+            tsa.gather_kv(sp, db.k_pool, db.v_pool, db.bt, ko, vo)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / reps
+        nbytes = 2 * 2 * n * wl.num_kv_heads * wl.head_dim * 2
+        res[f"gather_{name}"] = {"ms": ms, "bytes": nbytes, "gbs": nbytes / ms / 1e6}
+        del db, ko, vo
+        torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path is "
+              "sharded by KV head or by sequence with no exchange, see the design notes.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2607_17181_amd as tsa
+    import gpu_harness as harness
+    import workload
+
+    tsa.library()  # fail loudly if the HIP library is missing
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+
+    r = time_config(args.config, args.steps, args.warmup, torch, tsa, harness, workload)
+    wl = r.pop("wl")
+    r.pop("db")
+    achieved = r["prefill_tflops"]
+    line = {
+        "metric": METRIC,
+        "value": round(r["tflops_step"], 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": {"single": "single continuation: P=25,000 cached + S=2,048 new tokens, "
+                                   "Hq=8 Hkv=1 d=128, page 16, shuffled 100K-page pool",
+                         }.get(args.config, args.config),
+            "num_seqs": wl.num_seqs,
+            "prefix_lens": wl.prefix_lens.tolist() if wl.num_seqs <= 4 else "ragged",
+            "suffix_lens": wl.suffix_lens.tolist() if wl.num_seqs <= 4 else "ragged",
+            "num_q_heads": wl.num_q_heads, "num_kv_heads": wl.num_kv_heads,
+            "head_dim": wl.head_dim, "page_size": wl.page_size, "pool_pages": wl.num_pages,
+            "algorithmic_flops": r["flops"],
+        },
+        "pct_bf16_peak": round(100 * r["tflops_step"] / PEAK_BF16_TFLOPS, 2),
+        "ms_per_continuation": round(r["ms_per_step"] / wl.num_seqs, 4),
+        "breakdown_ms": {"plan_host": round(r["plan_us"] / 1e3, 4),
+                         "append_kv": round(r["append_ms"], 4),
+                         "prefill_call": round(r["prefill_call_ms"], 4)},
+        "roofline": {"bound": "mfma", "kernel": "prefill_kernel + combine_kernel (one prefill call)",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+    }
+    extra = {"main": r}
+    if args.extra_json:
+        extra["bandwidth"] = standalone_bandwidth(torch, tsa, harness, workload)
+        if args.all_configs:
+            for name in ("tiny", "ragged", "long", "cold"):
+                if name == args.config:
+                    continue
+                rr = time_config(name, max(5, args.steps // 5), 2, torch, tsa, harness, workload)
+                rr.pop("wl")
+                rr.pop("db")
+                extra[name] = rr
+                torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        import oracle
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, oracle, harness)
+    if args.extra_json:
+        with open(args.extra_json, "w") as f:
+            json.dump(extra, f, indent=1, default=float)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -5,21 +5,35 @@
 //
 // One workgroup (4 waves, 256 threads) runs one work item of the plan: a
 // query tile of 256 rows -- tile_tokens new tokens times the `group` query
-// heads that share one KV head, so every K/V byte staged in LDS serves all
-// of them -- against one contiguous range of 64-key tiles.  Each wave owns
-// 64 rows as two 32-row MFMA blocks.
+// heads that share one KV head, so every K/V byte staged in LDS serves all of
+// them -- against one contiguous range of 64-key tiles.  Each wave owns 64
+// rows as two 32-row MFMA blocks; every K and V operand read from LDS feeds
+// both blocks.
 //
-// Per key tile:
-//   * page walk + 16-byte global loads of the next tile into registers
-//     (keys at or past P_b + S_b are zero-filled, never loaded);
-//   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (K from LDS, Q in registers);
-//   * causal mask only on tiles that cross the diagonal;
-//   * online softmax in base 2 with a lazy rescale: the running maximum is
-//     only moved (and O rescaled) when some row's new maximum exceeds it by
-//     more than 2^8, so exp2 arguments stay <= 8;
-//   * O^T += V^T P^T on the same MFMA, P converted to bf16 in registers
-//     (the S^T accumulator layout already is the B-operand layout);
-//   * the registers of the next tile go to the other LDS buffer.
+// Data movement.  K/V tiles move HBM -> LDS with global_load_lds_dwordx4
+// (no register staging), four tiles deep: each 1 KB wave-load stays inside
+// one page, so its page id is a wave-uniform scalar load of the block table
+// and the per-lane part of the address is loop-invariant.  Keys at or past
+// P_b + S_b are never fetched from unowned pages; V entries past the end are
+// zeroed in LDS so stale slots (even NaN) cannot reach the output.
+//   K tile in LDS: 64 keys x D, natural key order, 16-byte chunks XOR-swizzled
+//                  by row.
+//   V tile in LDS: per page, [D][span] (tokens innermost, as in the pool),
+//                  chunks XOR-swizzled by feature row.
+// The QK^T A-operand reads K rows in the order that swaps the middle quarters
+// of every 16 keys; with that order the S^T accumulator of lane half h holds
+// 8 consecutive keys per 16, which is exactly the B-operand layout the PV
+// MFMA needs, so P goes from accumulator to operand in registers and V needs
+// no transpose.
+//
+// Pipeline (per wave, one iteration per key tile t):
+//     O   += V(t-1)^T P(t-1)      32 x v_mfma_f32_32x32x16_bf16
+//     P(t) = softmax step on S(t)  VALU: max, permlane32 swap, fma, exp2,
+//                                  cvt_pk_bf16, fp32 row sums
+//     S(t+1) = K(t+1) Q^T          32 x MFMA
+// The softmax of one tile runs between the MFMAs of its neighbours.  The
+// running maximum is lazy: O and l are rescaled only when some row's maximum
+// grows by more than 2^8, so exp2 arguments stay <= 8.
 //
 // Items whose query tile is split over several key ranges write normalised
 // fp32 partials and base-2 LSE to the workspace; the combine kernel merges
@@ -36,136 +50,281 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_void;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
+constexpr int kStages = 4;
 
-template <int D>
-struct Smem {
-    static constexpr int KSTR = D + 8;  // K tile row stride (elements): 16-byte pad
-    static constexpr int VSTR = kKeysPerTile + 8;  // V^T tile row stride (elements)
-    uint16_t k[2][kKeysPerTile * KSTR];
-    uint16_t v[2][D * VSTR];
+struct NoMask {
+    static constexpr bool value = false;
+};
+struct WithMask {
+    static constexpr bool value = true;
 };
 
-// Position of key `kk` (0..15) inside its 16-key group in the V^T tile.
-// The S^T accumulator gives lane half h the keys {4h..4h+3, 8+4h..8+4h+3}
-// of each 16-key group; storing the middle two quarters swapped makes those
-// 8 keys contiguous, so the PV A-operand is one 16-byte LDS read.
-__device__ __forceinline__ int vt_pos(int kk) {
-    const int q = kk >> 2;
-    const int qs = (q == 1) ? 2 : (q == 2) ? 1 : q;
-    return (qs << 2) | (kk & 3);
+template <int D, int SPAN>
+struct Geo {
+    static constexpr int TILE_BYTES = kKeysPerTile * D * 2;  // one K (or V) tile
+    static constexpr int STAGE_BYTES = 2 * TILE_BYTES;
+    static constexpr int LOADS = TILE_BYTES / 1024 / 4;      // wave-loads per wave per tile
+    static constexpr int K_CH = D / 8;                       // 16-byte chunks per K row
+    static constexpr int K_RPL = 1024 / (2 * D);             // K rows per wave-load
+    static constexpr int V_CH = SPAN / 8;                    // chunks per V block row
+    static constexpr int V_RPL = 1024 / (2 * SPAN);          // V block rows per wave-load
+    static constexpr int V_BLOCK = 2 * D * SPAN;             // bytes of one page block
+    static constexpr int V_LPB = V_BLOCK / 1024;             // wave-loads per page block
+    static constexpr int KS = D / 16;                        // QK^T k-steps
+    static constexpr int DB = D / 32;                        // 32-wide output blocks
+    static_assert(V_LPB >= 1, "page block smaller than one wave-load");
+};
+
+// Chunk swizzles (bank-conflict-free MFMA operand reads).
+template <int D>
+__device__ __forceinline__ int kswz(int row) {
+    return D == 128 ? (row & 15) : ((row & 3) | ((row >> 1) & 4));
+}
+template <int SPAN>
+__device__ __forceinline__ int vswz(int d) {
+    if (SPAN == 8)
+        return 0;
+    if (SPAN == 16)
+        return ((d >> 2) ^ (d >> 3)) & 1;
+    if (SPAN == 32)
+        return (d >> 1) & 3;
+    return d & 7;
+}
+// QK^T A-operand row order: swap bits 2 and 3 (middle quarters of 16).
+__device__ __forceinline__ int pi_row(int i) {
+    return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1);
 }
 
-template <int D>
-struct TileRegs {
-    static constexpr int NK = (kKeysPerTile * D / 8) / 256;  // 16-byte K chunks per thread
-    static constexpr int NV = NK;                             // 16-byte V chunks per thread
-    u32x4 k[NK];
-    u32x4 v[NV];
-};
+__device__ __forceinline__ float xhalf_max(float x) {
+    // Lanes l and l^32 hold the two halves of one query row's keys.
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
-struct ItemCtx {
-    const int32_t* bt_row;  // block-table row of the sequence
-    int64_t kv_head_off;    // g * (ps * D): offset of the head inside a page
-    int kv_len;             // P_b + S_b
+__device__ __forceinline__ void wait_vmem_all() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+struct Ctx {
+    const char* kpool_g;      // K pool + head offset (bytes)
+    const char* vpool_g;      // V pool + head offset (bytes)
+    const int32_t* bt_row;    // block-table row of the sequence
+    int64_t page_bytes;       // bytes per page (all heads)
+    int kv_len;               // P_b + S_b
     int page_shift;
     int ps;
-    int hkv;
 };
 
-// Issue the global loads of key tile `kt` into registers.
-template <int D>
-__device__ __forceinline__ void load_tile(TileRegs<D>& r, const ItemCtx& c, int kt,
-                                          const uint16_t* __restrict__ k_pool,
-                                          const uint16_t* __restrict__ v_pool) {
-    const int tid = threadIdx.x;
-    const int k0 = kt * kKeysPerTile;
-    constexpr int CH = D / 8;
+template <int D, int SPAN>
+struct Loader {
+    uint32_t koff[Geo<D, SPAN>::LOADS];  // per-lane byte offsets (loop-invariant)
+    uint32_t voff[Geo<D, SPAN>::LOADS];
+    int wave;
+
+    __device__ __forceinline__ void init(int w, int lane, int ps) {
+        using G = Geo<D, SPAN>;
+        wave = w;
 #pragma unroll
-    for (int i = 0; i < TileRegs<D>::NK; ++i) {
-        const int ch = tid + 256 * i;
-        const int pos = k0 + ch / CH;
-        const int col = ch % CH;
-        if (pos < c.kv_len) {
-            const int64_t page = c.bt_row[pos >> c.page_shift];
-            const uint16_t* src = k_pool + (page * c.hkv) * ((int64_t)c.ps * D) + c.kv_head_off +
-                                  (int64_t)(pos & (c.ps - 1)) * D + col * 8;
-            r.k[i] = *reinterpret_cast<const u32x4*>(src);
-        } else {
-            r.k[i] = u32x4{0, 0, 0, 0};
+        for (int i = 0; i < G::LOADS; ++i) {
+            const int li = w * G::LOADS + i;
+            const int row = li * G::K_RPL + lane / G::K_CH;
+            const int lc = (lane % G::K_CH) ^ kswz<D>(row);
+            koff[i] = (uint32_t)(((lane / G::K_CH) * D + lc * 8) * 2);
+            const int bl = li % G::V_LPB;
+            const int d = bl * G::V_RPL + lane / G::V_CH;
+            const int vlc = (lane % G::V_CH) ^ vswz<SPAN>(d);
+            voff[i] = (uint32_t)(((lane / G::V_CH) * ps + vlc * 8) * 2);
         }
     }
-    // V chunk = 8 consecutive keys of one feature row inside one page.
-    const int span = c.ps < kKeysPerTile ? c.ps : kKeysPerTile;  // keys of one page in the tile
-    const int gpp = span >> 3;                                   // 8-key groups per page row
+
+    // Issue the direct-to-LDS loads of key tile starting at k0 into `stage`.
+    __device__ __forceinline__ void issue(char* stage, int k0, const Ctx& c) const {
+        using G = Geo<D, SPAN>;
 #pragma unroll
-    for (int i = 0; i < TileRegs<D>::NV; ++i) {
-        const int ch = tid + 256 * i;
-        const int grp = ch % gpp;
-        const int d = (ch / gpp) % D;
-        const int pj = ch / (gpp * D);
-        const int pos = k0 + pj * span + grp * 8;
-        if (pos < c.kv_len) {
-            const int64_t page = c.bt_row[pos >> c.page_shift];
-            const uint16_t* src = v_pool + (page * c.hkv) * ((int64_t)c.ps * D) + c.kv_head_off +
-                                  (int64_t)d * c.ps + (pos & (c.ps - 1));
-            u32x4 x = *reinterpret_cast<const u32x4*>(src);
-            const int valid = c.kv_len - pos;  // zero slots at or past the end
-            if (valid < 8) {
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const int e = 2 * w;
-                    uint32_t m = (e < valid ? 0x0000FFFFu : 0u) | (e + 1 < valid ? 0xFFFF0000u : 0u);
-                    x[w] &= m;
-                }
+        for (int i = 0; i < G::LOADS; ++i) {
+            const int li = wave * G::LOADS + i;
+            const int key0 = k0 + li * G::K_RPL;
+            if (key0 < c.kv_len) {
+                const int64_t page = c.bt_row[key0 >> c.page_shift];
+                const char* src = c.kpool_g + page * c.page_bytes +
+                                  (int64_t)(key0 & (c.ps - 1)) * (D * 2) + koff[i];
+                __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)(stage + li * 1024),
+                                                 16, 0, 0);
             }
-            r.v[i] = x;
-        } else {
-            r.v[i] = u32x4{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int i = 0; i < G::LOADS; ++i) {
+            const int li = wave * G::LOADS + i;
+            const int pj = li / G::V_LPB;
+            const int bl = li % G::V_LPB;
+            const int key0 = k0 + pj * SPAN;
+            if (key0 < c.kv_len) {
+                const int64_t page = c.bt_row[key0 >> c.page_shift];
+                const char* src = c.vpool_g + page * c.page_bytes +
+                                  (int64_t)(bl * G::V_RPL) * c.ps * 2 +
+                                  (int64_t)(key0 & (c.ps - 1)) * 2 + voff[i];
+                __builtin_amdgcn_global_load_lds(
+                    (gbl_void*)src, (lds_void*)(stage + G::TILE_BYTES + li * 1024), 16, 0, 0);
+            }
+        }
+    }
+};
+
+// Zero the V entries of keys kv_len .. k0+63 of the tile in `stage`.
+template <int D, int SPAN>
+__device__ __forceinline__ void zero_v_tail(char* stage, int k0, int kv_len) {
+    using G = Geo<D, SPAN>;
+    const int first = kv_len - k0;  // first key (tile-relative) past the end
+    if (first >= kKeysPerTile)
+        return;
+    const int ntail = kKeysPerTile - first;
+    uint16_t* v = reinterpret_cast<uint16_t*>(stage + G::TILE_BYTES);
+    for (int e = threadIdx.x; e < D * ntail; e += 256) {
+        const int d = e / ntail;
+        const int key = first + e % ntail;
+        const int pj = key / SPAN, inb = key % SPAN;
+        const int phys = (inb >> 3) ^ vswz<SPAN>(d);
+        v[(pj * G::V_BLOCK + d * SPAN * 2 + phys * 16) / 2 + (inb & 7)] = 0;
+    }
+}
+
+// S^T = K Q^T for both 32-row blocks of the wave.
+template <int D, int SPAN>
+__device__ __forceinline__ void qk_tile(f32x16 (&s)[2][2], const char* stage,
+                                        const bf16x8 (&qf)[2][D / 16], int lq, int lh) {
+    using G = Geo<D, SPAN>;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+            s[qb][kb] = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < G::KS; ++ks) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const int row = kb * 32 + pi_row(lq);
+            const int lc = 2 * ks + lh;
+            const u32x4 a = *reinterpret_cast<const u32x4*>(
+                stage + row * (2 * D) + ((lc ^ kswz<D>(row)) << 4));
+            const bf16x8 af = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb)
+                s[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[qb][ks], s[qb][kb],
+                                                                    0, 0, 0);
         }
     }
 }
 
-template <int D>
-__device__ __forceinline__ void store_tile(Smem<D>& sm, int buf, const TileRegs<D>& r,
-                                           const ItemCtx& c) {
-    const int tid = threadIdx.x;
-    constexpr int CH = D / 8;
+// O^T += V^T P^T for both 32-row blocks.
+template <int D, int SPAN>
+__device__ __forceinline__ void pv_tile(f32x16 (&o)[2][D / 32], const char* stage,
+                                        const bf16x8 (&pf)[2][4], int lq, int lh) {
+    using G = Geo<D, SPAN>;
+    const char* vt = stage + G::TILE_BYTES;
 #pragma unroll
-    for (int i = 0; i < TileRegs<D>::NK; ++i) {
-        const int ch = tid + 256 * i;
-        const int key = ch / CH, col = ch % CH;
-        *reinterpret_cast<u32x4*>(&sm.k[buf][key * Smem<D>::KSTR + col * 8]) = r.k[i];
-    }
-    const int span = c.ps < kKeysPerTile ? c.ps : kKeysPerTile;
-    const int gpp = span >> 3;
+    for (int ks2 = 0; ks2 < 4; ++ks2) {
+        const int key = 16 * ks2 + 8 * lh;
+        const int pj = key / SPAN, lc = (key % SPAN) >> 3;
 #pragma unroll
-    for (int i = 0; i < TileRegs<D>::NV; ++i) {
-        const int ch = tid + 256 * i;
-        const int grp = ch % gpp;
-        const int d = (ch / gpp) % D;
-        const int pj = ch / (gpp * D);
-        const int key0 = pj * span + grp * 8;  // multiple of 8
-        const int base = (key0 & ~15);
-        const int kk = key0 & 15;  // 0 or 8
-        uint16_t* row = &sm.v[buf][d * Smem<D>::VSTR + base];
-        *reinterpret_cast<u32x2*>(row + vt_pos(kk)) = u32x2{r.v[i][0], r.v[i][1]};
-        *reinterpret_cast<u32x2*>(row + vt_pos(kk + 4)) = u32x2{r.v[i][2], r.v[i][3]};
+        for (int db = 0; db < G::DB; ++db) {
+            const int d = db * 32 + lq;
+            const u32x4 a = *reinterpret_cast<const u32x4*>(
+                vt + pj * G::V_BLOCK + d * (SPAN * 2) + ((lc ^ vswz<SPAN>(d)) << 4));
+            const bf16x8 af = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb)
+                o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[qb][ks2], o[qb][db],
+                                                                    0, 0, 0);
+        }
     }
 }
 
-__device__ __forceinline__ float wave_xor32(float x) {
-    return __shfl_xor(x, 32);
+// One online-softmax step on S(t): returns P(t) as bf16 B-operands, updates
+// the running max / row sums, and reports whether O must be rescaled by
+// alpha before P(t) is accumulated.
+template <bool MASK>
+__device__ __forceinline__ bool softmax_tile(f32x16 (&s)[2][2], bf16x8 (&pf)[2][4],
+                                             float (&m_run)[2], float (&l_run)[2],
+                                             float (&alpha)[2], float scale, int k0,
+                                             const int (&qpos)[2], int lh) {
+    if (MASK) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int key = k0 + 32 * kb + 16 * (j >> 3) + 8 * lh + (j & 7);
+                    if (key > qpos[qb])
+                        s[qb][kb][j] = -INFINITY;
+                }
+    }
+    float mt[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        float m = fmaxf(s[qb][0][0], s[qb][0][1]);
+#pragma unroll
+        for (int j = 2; j < 16; j += 2)
+            m = fmaxf(m, fmaxf(s[qb][0][j], s[qb][0][j + 1]));
+#pragma unroll
+        for (int j = 0; j < 16; j += 2)
+            m = fmaxf(m, fmaxf(s[qb][1][j], s[qb][1][j + 1]));
+        mt[qb] = xhalf_max(m) * scale;
+    }
+    const bool grow = (mt[0] > m_run[0] + kRescaleThreshold) ||
+                      (mt[1] > m_run[1] + kRescaleThreshold);
+    const bool resc = __any(grow);
+    if (resc) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            const float mn = fmaxf(m_run[qb], mt[qb]);
+            alpha[qb] = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - mn);
+            m_run[qb] = mn;
+            l_run[qb] *= alpha[qb];
+        }
+    }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float mb = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
+        float ls = l_run[qb];
+#pragma unroll
+        for (int ks2 = 0; ks2 < 4; ++ks2) {
+            bf16x8 v;
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(
+                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e], scale, -mb));
+                const float p1 = __builtin_amdgcn_exp2f(
+                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e + 1], scale, -mb));
+                ls += p0;
+                ls += p1;
+                v[e] = (__bf16)p0;
+                v[e + 1] = (__bf16)p1;
+            }
+            pf[qb][ks2] = v;
+        }
+        l_run[qb] = ls;
+    }
+    return resc;
 }
 
-template <int D>
+template <int D, int SPAN>
 __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ k_pool,
                                                          const uint16_t* __restrict__ v_pool,
@@ -174,190 +333,136 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
                                                          float* __restrict__ lse,
                                                          float* __restrict__ part_o,
                                                          float* __restrict__ part_lse) {
-    __shared__ Smem<D> sm;
-    constexpr int KS = D / 16;  // MFMA k-steps over the head dimension
-    constexpr int DB = D / 32;  // 32-wide output blocks over the head dimension
+    using G = Geo<D, SPAN>;
+    __shared__ __attribute__((aligned(1024))) char smem[kStages * G::STAGE_BYTES];
 
     const WorkItem w = decode_item(p, blockIdx.x);
     const SeqDesc s = p.seq[w.seq];
-    const int G = p.group;
+    const int Gq = p.group;
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lq = lane & 31;
     const int lh = lane >> 5;
 
-    ItemCtx c;
+    Ctx c;
+    c.page_bytes = (int64_t)p.num_kv_heads * p.page_size * D * 2;
+    c.kpool_g = reinterpret_cast<const char*>(k_pool) + (int64_t)w.kv_head * p.page_size * D * 2;
+    c.vpool_g = reinterpret_cast<const char*>(v_pool) + (int64_t)w.kv_head * p.page_size * D * 2;
     c.bt_row = bt + (int64_t)w.seq * p.bt_stride;
-    c.kv_head_off = (int64_t)w.kv_head * p.page_size * D;
     c.kv_len = s.prefix_len + s.suffix_len;
     c.page_shift = p.page_shift;
     c.ps = p.page_size;
-    c.hkv = p.num_kv_heads;
+
+    Loader<D, SPAN> ld;
+    ld.init(wave, lane, c.ps);
+
+    const int tb = w.tile_begin, te = w.tile_end;
+    auto stage_ptr = [&](int t) -> char* { return smem + (t & (kStages - 1)) * G::STAGE_BYTES; };
+
+    // Prologue loads: tiles tb, tb+1 (tile tb+2 is issued after the first wait).
+    if (tb < te)
+        ld.issue(stage_ptr(tb), tb * kKeysPerTile, c);
+    if (tb + 1 < te)
+        ld.issue(stage_ptr(tb + 1), (tb + 1) * kKeysPerTile, c);
 
     // Query rows of this lane: one per 32-row block.
-    const int rows_used = p.tile_tokens * G;
-    int qtok[2];   // token index inside the tile, or -1 for a padding row
-    int qhead[2];
-    bf16x8 qf[2][KS];
+    const int rows_used = p.tile_tokens * Gq;
+    int qtok[2], qhead[2], qpos[2];
+    bf16x8 qf[2][G::KS];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const int r = wave * 64 + qb * 32 + lq;
-        const int t = r / G;
+        const int t = r / Gq;
         const bool valid = r < rows_used && t < w.num_tokens;
         qtok[qb] = valid ? t : -1;
-        qhead[qb] = w.kv_head * G + r % G;
+        qhead[qb] = w.kv_head * Gq + r % Gq;
+        qpos[qb] = s.prefix_len + w.first_token + (valid ? t : w.num_tokens - 1);
         const uint16_t* src = q + ((int64_t)(s.tok_off + w.first_token + t) * p.num_q_heads +
                                    qhead[qb]) * D + lh * 8;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        for (int ks = 0; ks < G::KS; ++ks) {
             u32x4 x = valid ? *reinterpret_cast<const u32x4*>(src + ks * 16) : u32x4{0, 0, 0, 0};
             qf[qb][ks] = __builtin_bit_cast(bf16x8, x);
         }
     }
-    // Absolute position of each row's token (padding rows: the tile's last).
-    int qpos[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
-        qpos[qb] = s.prefix_len + w.first_token + (qtok[qb] >= 0 ? qtok[qb] : w.num_tokens - 1);
-    const int tile_first_pos = s.prefix_len + w.first_token;
 
     const float scale = sm_scale * kLog2e;  // logits in base-2 units
-    f32x16 o[2][DB];
+    f32x16 o[2][G::DB];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+        for (int db = 0; db < G::DB; ++db)
             o[qb][db] = f32x16{};
-    float m_run[2] = {-INFINITY, -INFINITY};  // running max of scaled logits
-    float l_run[2] = {0.f, 0.f};              // this lane's partial row sum
+    float m_run[2] = {-INFINITY, -INFINITY};
+    float l_run[2] = {0.f, 0.f};   // this lane's partial row sums
+    float alpha[2] = {1.f, 1.f};
+    bool resc = false;
 
-    TileRegs<D> regs;
-    if (w.tile_begin < w.tile_end) {
-        load_tile<D>(regs, c, w.tile_begin, k_pool, v_pool);
-        store_tile<D>(sm, 0, regs, c);
-    }
+    wait_vmem_all();
     __syncthreads();
+    if (tb < te)
+        zero_v_tail<D, SPAN>(stage_ptr(tb), tb * kKeysPerTile, c.kv_len);
+    if (tb + 1 < te)
+        zero_v_tail<D, SPAN>(stage_ptr(tb + 1), (tb + 1) * kKeysPerTile, c.kv_len);
+    if (tb + 2 < te)
+        ld.issue(stage_ptr(tb + 2), (tb + 2) * kKeysPerTile, c);
 
-    for (int kt = w.tile_begin; kt < w.tile_end; ++kt) {
-        const int cur = (kt - w.tile_begin) & 1;
-        const bool has_next = kt + 1 < w.tile_end;
-        if (has_next)
-            load_tile<D>(regs, c, kt + 1, k_pool, v_pool);
+    f32x16 sc[2][2];
+    bf16x8 pf[2][4];
+    if (tb < te)
+        qk_tile<D, SPAN>(sc, stage_ptr(tb), qf, lq, lh);
 
-        // S^T = K Q^T: acc[qb][kb] holds 32 keys x 32 queries.
-        f32x16 sacc[2][2];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-                sacc[qb][kb] = f32x16{};
-        const uint16_t* ktile = sm.k[cur];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                const u32x4 a = *reinterpret_cast<const u32x4*>(
-                    &ktile[(kb * 32 + lq) * Smem<D>::KSTR + ks * 16 + lh * 8]);
-                const bf16x8 af = __builtin_bit_cast(bf16x8, a);
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb)
-                    sacc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[qb][ks],
-                                                                           sacc[qb][kb], 0, 0, 0);
-            }
-        }
+    // First tile whose keys can lie past some row of the tile (needs the mask).
+    const int tile_first_pos = s.prefix_len + w.first_token;
+    // tmask = smallest t with t * 64 + 63 > tile_first_pos.
+    const int tmask = tile_first_pos < kKeysPerTile - 1
+                          ? 0 : (tile_first_pos - (kKeysPerTile - 1)) / kKeysPerTile + 1;
 
-        // Causal mask, only on tiles that cross the diagonal.
-        const int k0 = kt * kKeysPerTile;
-        if (k0 + kKeysPerTile - 1 > tile_first_pos) {
+    auto iteration = [&](int t, auto mask_tag) {
+        constexpr bool MASK = decltype(mask_tag)::value;
+        if (resc) {  // rescale decided on S(t-1): before P(t-1) is accumulated
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int j = 0; j < 16; ++j) {
-                        const int key = k0 + kb * 32 + 8 * (j >> 2) + 4 * lh + (j & 3);
-                        if (key > qpos[qb])
-                            sacc[qb][kb][j] = -INFINITY;
-                    }
+                for (int db = 0; db < G::DB; ++db)
+                    o[qb][db] *= alpha[qb];
         }
-
-        // Row maxima in base-2 units (each row's 64 keys live in lanes lq
-        // and lq+32; the scale is positive, so it commutes with max).
-        float mt[2];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            float m = sacc[qb][0][0];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    m = fmaxf(m, sacc[qb][kb][j]);
-            mt[qb] = fmaxf(m, wave_xor32(m)) * scale;
-        }
-        // Lazy rescale: only when some row's max grew by more than the threshold.
-        const bool grow = (mt[0] > m_run[0] + kRescaleThreshold) ||
-                          (mt[1] > m_run[1] + kRescaleThreshold);
-        if (__any(grow)) {
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                const float mn = fmaxf(m_run[qb], mt[qb]);
-                const float alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - mn);
-                m_run[qb] = mn;
-                l_run[qb] *= alpha;
-#pragma unroll
-                for (int db = 0; db < DB; ++db)
-                    o[qb][db] *= alpha;
-            }
-        }
-
-        // P = exp2(S - m) in bf16, laid out as the B operand of O^T += V^T P^T.
-        bf16x8 pf[2][4];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            const float mb = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
-            float ls = 0.f;
-#pragma unroll
-            for (int ks2 = 0; ks2 < 4; ++ks2) {
-                bf16x8 v;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float pe = __builtin_amdgcn_exp2f(
-                        fmaf(sacc[qb][ks2 >> 1][(ks2 & 1) * 8 + e], scale, -mb));
-                    ls += pe;
-                    v[e] = (__bf16)pe;
-                }
-                pf[qb][ks2] = v;
-            }
-            l_run[qb] += ls;
-        }
-
-        // O^T += V^T P^T.
-        const uint16_t* vtile = sm.v[cur];
-#pragma unroll
-        for (int ks2 = 0; ks2 < 4; ++ks2) {
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const u32x4 a = *reinterpret_cast<const u32x4*>(
-                    &vtile[(db * 32 + lq) * Smem<D>::VSTR + ks2 * 16 + lh * 8]);
-                const bf16x8 af = __builtin_bit_cast(bf16x8, a);
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb)
-                    o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[qb][ks2],
-                                                                        o[qb][db], 0, 0, 0);
-            }
-        }
-
-        if (has_next)
-            store_tile<D>(sm, cur ^ 1, regs, c);
+        if (t > tb)
+            pv_tile<D, SPAN>(o, stage_ptr(t - 1), pf, lq, lh);
+        resc = softmax_tile<MASK>(sc, pf, m_run, l_run, alpha, scale, t * kKeysPerTile, qpos, lh);
+        if (t + 1 < te)
+            qk_tile<D, SPAN>(sc, stage_ptr(t + 1), qf, lq, lh);
+        wait_vmem_all();
         __syncthreads();
+        if (t + 3 < te)
+            ld.issue(stage_ptr(t + 3), (t + 3) * kKeysPerTile, c);
+        if (t + 2 < te)
+            zero_v_tail<D, SPAN>(stage_ptr(t + 2), (t + 2) * kKeysPerTile, c.kv_len);
+    };
+
+    const int split = tmask < tb ? tb : (tmask > te ? te : tmask);
+    for (int t = tb; t < split; ++t)
+        iteration(t, NoMask{});
+    for (int t = split; t < te; ++t)
+        iteration(t, WithMask{});
+
+    if (tb < te) {
+        if (resc) {
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                for (int db = 0; db < G::DB; ++db)
+                    o[qb][db] *= alpha[qb];
+        }
+        pv_tile<D, SPAN>(o, stage_ptr(te - 1), pf, lq, lh);
     }
 
     // Epilogue: full row sums, normalise, write.
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        const float l = l_run[qb] + wave_xor32(l_run[qb]);
+        const float l = xhalf_sum(l_run[qb]);
         const float inv = l > 0.f ? 1.f / l : 0.f;
-        const float lse2 = l > 0.f ? m_run[qb] + log2f(l) : -INFINITY;
+        const float lse2 = l > 0.f ? m_run[qb] + __log2f(l) : -INFINITY;
         if (qtok[qb] < 0)
             continue;
         const int r = wave * 64 + qb * 32 + lq;
@@ -366,7 +471,7 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
                                 qhead[qb];
             uint16_t* dst = out + row * D;
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+            for (int db = 0; db < G::DB; ++db)
 #pragma unroll
                 for (int j4 = 0; j4 < 4; ++j4) {
                     bf16x4 v;
@@ -380,7 +485,7 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
         } else {
             float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D;
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+            for (int db = 0; db < G::DB; ++db)
 #pragma unroll
                 for (int j4 = 0; j4 < 4; ++j4) {
                     f32x4 v;
@@ -395,8 +500,9 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
     }
 }
 
-// Merge the split partials of one query tile (launched per work item; only
-// split 0 of a split tile does work).  Base-2 LSE merge in split order.
+// Merge the split partials of one query tile.  Grid: (work item, row chunk of
+// 8 rows); only split 0 of a split tile does work.  Base-2 LSE merge in
+// split order.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* __restrict__ part_o,
                                                       const float* __restrict__ part_lse,
@@ -405,41 +511,47 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
     const WorkItem w = decode_item(p, blockIdx.x);
     if (w.part_index < 0 || w.split != 0)
         return;
-    const SeqDesc s = p.seq[w.seq];
+    constexpr int TPR = D / 4;      // threads per row (4 features each)
+    constexpr int RPB = 256 / TPR;  // rows per block
+    const int r = blockIdx.y * RPB + threadIdx.x / TPR;
     const int G = p.group;
+    if (r >= w.num_tokens * G)
+        return;
+    const SeqDesc s = p.seq[w.seq];
     const int n = w.num_splits;
-    constexpr int TPR = D / 4;            // threads per row (4 features each)
-    constexpr int RPP = 256 / TPR;        // rows per pass
     const int sub = threadIdx.x % TPR;
-    const int rows = w.num_tokens * G;
-    for (int r = threadIdx.x / TPR; r < rows; r += RPP) {
-        float mx = -INFINITY;
-        for (int k = 0; k < n; ++k)
-            mx = fmaxf(mx, part_lse[(int64_t)(w.part_index + k) * kRowsPerTile + r]);
-        float acc[4] = {0.f, 0.f, 0.f, 0.f};
-        float wsum = 0.f;
-        for (int k = 0; k < n; ++k) {
-            const float lk = part_lse[(int64_t)(w.part_index + k) * kRowsPerTile + r];
-            const float wk = (lk == -INFINITY) ? 0.f : exp2f(lk - mx);
-            wsum += wk;
-            const f32x4 v = *reinterpret_cast<const f32x4*>(
-                part_o + ((int64_t)(w.part_index + k) * kRowsPerTile + r) * D + sub * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                acc[e] += wk * v[e];
-        }
-        const float inv = 1.f / wsum;
-        const int t = r / G;
-        const int64_t row = (int64_t)(s.tok_off + w.first_token + t) * p.num_q_heads +
-                            w.kv_head * G + r % G;
-        bf16x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            v[e] = (__bf16)(acc[e] * inv);
-        *reinterpret_cast<bf16x4*>(out + row * D + sub * 4) = v;
-        if (lse && sub == 0)
-            lse[row] = (mx + log2f(wsum)) * kLn2;
+    float mx = -INFINITY;
+    for (int k = 0; k < n; ++k)
+        mx = fmaxf(mx, part_lse[(int64_t)(w.part_index + k) * kRowsPerTile + r]);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    float wsum = 0.f;
+    for (int k = 0; k < n; ++k) {
+        const float lk = part_lse[(int64_t)(w.part_index + k) * kRowsPerTile + r];
+        const float wk = (lk == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk - mx);
+        wsum += wk;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(
+            part_o + ((int64_t)(w.part_index + k) * kRowsPerTile + r) * D + sub * 4);
+        acc += wk * v;
     }
+    const float inv = 1.f / wsum;
+    const int t = r / G;
+    const int64_t row = (int64_t)(s.tok_off + w.first_token + t) * p.num_q_heads +
+                        w.kv_head * G + r % G;
+    bf16x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        v[e] = (__bf16)(acc[e] * inv);
+    *reinterpret_cast<bf16x4*>(out + row * D + sub * 4) = v;
+    if (lse && sub == 0)
+        lse[row] = (mx + __log2f(wsum)) * kLn2;
+}
+
+template <int D, int SPAN>
+void launch_prefill_kernel(const PlanData& p, const uint16_t* q, const uint16_t* kp,
+                           const uint16_t* vp, const int32_t* bt, float sm_scale, uint16_t* out,
+                           float* lse, float* part_o, float* part_lse, hipStream_t st) {
+    hipLaunchKernelGGL((prefill_kernel<D, SPAN>), dim3(p.num_items), dim3(256), 0, st, p, q, kp,
+                       vp, bt, sm_scale, out, lse, part_o, part_lse);
 }
 
 template <int D>
@@ -448,13 +560,26 @@ int launch_prefill(const PlanData& p, const uint16_t* q, const uint16_t* kp, con
                    hipStream_t st) {
     float* part_o = reinterpret_cast<float*>(ws);
     float* part_lse = ws ? reinterpret_cast<float*>(ws + p.ws_lse_offset) : nullptr;
-    hipLaunchKernelGGL(prefill_kernel<D>, dim3(p.num_items), dim3(256), 0, st, p, q, kp, vp, bt,
-                       sm_scale, out, lse, part_o, part_lse);
+    switch (p.page_size) {
+    case 8:
+        launch_prefill_kernel<D, 8>(p, q, kp, vp, bt, sm_scale, out, lse, part_o, part_lse, st);
+        break;
+    case 16:
+        launch_prefill_kernel<D, 16>(p, q, kp, vp, bt, sm_scale, out, lse, part_o, part_lse, st);
+        break;
+    case 32:
+        launch_prefill_kernel<D, 32>(p, q, kp, vp, bt, sm_scale, out, lse, part_o, part_lse, st);
+        break;
+    default:
+        launch_prefill_kernel<D, 64>(p, q, kp, vp, bt, sm_scale, out, lse, part_o, part_lse, st);
+        break;
+    }
     int status = launch_status("prefill");
     if (status != TALARIA_SP_OK || p.num_part_items == 0)
         return status;
-    hipLaunchKernelGGL(combine_kernel<D>, dim3(p.num_items), dim3(256), 0, st, p, part_o,
-                       part_lse, out, lse);
+    constexpr int RPB = 256 / (D / 4);
+    hipLaunchKernelGGL(combine_kernel<D>, dim3(p.num_items, kRowsPerTile / RPB), dim3(256), 0, st,
+                       p, part_o, part_lse, out, lse);
     return launch_status("combine");
 }
 

@@ -69,11 +69,13 @@ struct WithMask {
     static constexpr bool value = true;
 };
 
-template <int D, int SPAN>
+template <int D, int SPAN, int QB>
 struct Geo {
+    static constexpr int NW = kRowsPerTile / (32 * QB);      // waves per workgroup
+    static constexpr int NT = 64 * NW;                       // threads per workgroup
     static constexpr int TILE_BYTES = kKeysPerTile * D * 2;  // one K (or V) tile
     static constexpr int STAGE_BYTES = 2 * TILE_BYTES;
-    static constexpr int LOADS = TILE_BYTES / 1024 / 4;      // wave-loads per wave per tile
+    static constexpr int LOADS = TILE_BYTES / 1024 / NW;     // wave-loads per wave per tile
     static constexpr int K_CH = D / 8;                       // 16-byte chunks per K row
     static constexpr int K_RPL = 1024 / (2 * D);             // K rows per wave-load
     static constexpr int V_CH = SPAN / 8;                    // chunks per V block row
@@ -83,6 +85,8 @@ struct Geo {
     static constexpr int KS = D / 16;                        // QK^T k-steps
     static constexpr int DB = D / 32;                        // 32-wide output blocks
     static_assert(V_LPB >= 1, "page block smaller than one wave-load");
+    static_assert(LOADS >= 1, "fewer wave-loads than waves");
+    static_assert(NT == 2 * kRowsPerTile / QB, "launch bounds mismatch");
 };
 
 // Chunk swizzles (bank-conflict-free MFMA operand reads).
@@ -131,14 +135,14 @@ struct Ctx {
     int ps;
 };
 
-template <int D, int SPAN>
+template <int D, int SPAN, int QB>
 struct Loader {
-    uint32_t koff[Geo<D, SPAN>::LOADS];  // per-lane byte offsets (loop-invariant)
-    uint32_t voff[Geo<D, SPAN>::LOADS];
+    using G = Geo<D, SPAN, QB>;
+    uint32_t koff[G::LOADS];  // per-lane byte offsets (loop-invariant)
+    uint32_t voff[G::LOADS];
     int wave;
 
     __device__ __forceinline__ void init(int w, int lane, int ps) {
-        using G = Geo<D, SPAN>;
         wave = w;
 #pragma unroll
         for (int i = 0; i < G::LOADS; ++i) {
@@ -153,9 +157,8 @@ struct Loader {
         }
     }
 
-    // Issue the direct-to-LDS loads of key tile starting at k0 into `stage`.
+    // Issue the direct-to-LDS loads of the key tile starting at k0 into `stage`.
     __device__ __forceinline__ void issue(char* stage, int k0, const Ctx& c) const {
-        using G = Geo<D, SPAN>;
 #pragma unroll
         for (int i = 0; i < G::LOADS; ++i) {
             const int li = wave * G::LOADS + i;
@@ -187,15 +190,15 @@ struct Loader {
 };
 
 // Zero the V entries of keys kv_len .. k0+63 of the tile in `stage`.
-template <int D, int SPAN>
+template <int D, int SPAN, int QB>
 __device__ __forceinline__ void zero_v_tail(char* stage, int k0, int kv_len) {
-    using G = Geo<D, SPAN>;
+    using G = Geo<D, SPAN, QB>;
     const int first = kv_len - k0;  // first key (tile-relative) past the end
     if (first >= kKeysPerTile)
         return;
     const int ntail = kKeysPerTile - first;
     uint16_t* v = reinterpret_cast<uint16_t*>(stage + G::TILE_BYTES);
-    for (int e = threadIdx.x; e < D * ntail; e += 256) {
+    for (int e = threadIdx.x; e < D * ntail; e += G::NT) {
         const int d = e / ntail;
         const int key = first + e % ntail;
         const int pj = key / SPAN, inb = key % SPAN;
@@ -204,18 +207,17 @@ __device__ __forceinline__ void zero_v_tail(char* stage, int k0, int kv_len) {
     }
 }
 
-// S^T = K Q^T for both 32-row blocks of the wave.
-template <int D, int SPAN>
-__device__ __forceinline__ void qk_tile(f32x16 (&s)[2][2], const char* stage,
-                                        const bf16x8 (&qf)[2][D / 16], int lq, int lh) {
-    using G = Geo<D, SPAN>;
+// S^T = K Q^T for the wave's QB 32-row blocks.
+template <int D, int SPAN, int QB>
+__device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* stage,
+                                        const bf16x8 (&qf)[QB][D / 16], int lq, int lh) {
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
             s[qb][kb] = f32x16{};
 #pragma unroll
-    for (int ks = 0; ks < G::KS; ++ks) {
+    for (int ks = 0; ks < D / 16; ++ks) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             const int row = kb * 32 + pi_row(lq);
@@ -224,48 +226,52 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[2][2], const char* stage,
                 stage + row * (2 * D) + ((lc ^ kswz<D>(row)) << 4));
             const bf16x8 af = __builtin_bit_cast(bf16x8, a);
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
                 s[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[qb][ks], s[qb][kb],
                                                                     0, 0, 0);
         }
     }
 }
 
-// O^T += V^T P^T for both 32-row blocks.
-template <int D, int SPAN>
-__device__ __forceinline__ void pv_tile(f32x16 (&o)[2][D / 32], const char* stage,
-                                        const bf16x8 (&pf)[2][4], int lq, int lh) {
-    using G = Geo<D, SPAN>;
+// O^T += V^T P^T for the wave's QB 32-row blocks.
+template <int D, int SPAN, int QB>
+__device__ __forceinline__ void pv_tile(f32x16 (&o)[QB][D / 32], const char* stage,
+                                        const bf16x8 (&pf)[QB][4], int lq, int lh) {
+    using G = Geo<D, SPAN, QB>;
     const char* vt = stage + G::TILE_BYTES;
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
         const int key = 16 * ks2 + 8 * lh;
         const int pj = key / SPAN, lc = (key % SPAN) >> 3;
 #pragma unroll
-        for (int db = 0; db < G::DB; ++db) {
+        for (int db = 0; db < D / 32; ++db) {
             const int d = db * 32 + lq;
             const u32x4 a = *reinterpret_cast<const u32x4*>(
                 vt + pj * G::V_BLOCK + d * (SPAN * 2) + ((lc ^ vswz<SPAN>(d)) << 4));
             const bf16x8 af = __builtin_bit_cast(bf16x8, a);
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
                 o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[qb][ks2], o[qb][db],
                                                                     0, 0, 0);
         }
     }
 }
 
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+    return __builtin_fmaxf(a, __builtin_fmaxf(b, c));
+}
+
 // One online-softmax step on S(t): returns P(t) as bf16 B-operands, updates
 // the running max / row sums, and reports whether O must be rescaled by
 // alpha before P(t) is accumulated.
-template <bool MASK>
-__device__ __forceinline__ bool softmax_tile(f32x16 (&s)[2][2], bf16x8 (&pf)[2][4],
-                                             float (&m_run)[2], float (&l_run)[2],
-                                             float (&alpha)[2], float scale, int k0,
-                                             const int (&qpos)[2], int lh) {
+template <int QB, bool MASK>
+__device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB][4],
+                                             float (&m_run)[QB], float (&l_run)[QB],
+                                             float (&alpha)[QB], float scale, int k0,
+                                             const int (&qpos)[QB], int lh) {
     if (MASK) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -275,32 +281,34 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[2][2], bf16x8 (&pf)[2][
                         s[qb][kb][j] = -INFINITY;
                 }
     }
-    float mt[2];
+    float mt[QB];
+    bool grow = false;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        float m = fmaxf(s[qb][0][0], s[qb][0][1]);
+    for (int qb = 0; qb < QB; ++qb) {
+        float m = max3f(s[qb][0][0], s[qb][0][1], s[qb][0][2]);
 #pragma unroll
-        for (int j = 2; j < 16; j += 2)
-            m = fmaxf(m, fmaxf(s[qb][0][j], s[qb][0][j + 1]));
+        for (int j = 3; j < 15; j += 2)
+            m = max3f(m, s[qb][0][j], s[qb][0][j + 1]);
+        m = max3f(m, s[qb][0][15], s[qb][1][0]);
 #pragma unroll
-        for (int j = 0; j < 16; j += 2)
-            m = fmaxf(m, fmaxf(s[qb][1][j], s[qb][1][j + 1]));
+        for (int j = 1; j < 15; j += 2)
+            m = max3f(m, s[qb][1][j], s[qb][1][j + 1]);
+        m = __builtin_fmaxf(m, s[qb][1][15]);
         mt[qb] = xhalf_max(m) * scale;
+        grow = grow || (mt[qb] > m_run[qb] + kRescaleThreshold);
     }
-    const bool grow = (mt[0] > m_run[0] + kRescaleThreshold) ||
-                      (mt[1] > m_run[1] + kRescaleThreshold);
     const bool resc = __any(grow);
     if (resc) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            const float mn = fmaxf(m_run[qb], mt[qb]);
+        for (int qb = 0; qb < QB; ++qb) {
+            const float mn = __builtin_fmaxf(m_run[qb], mt[qb]);
             alpha[qb] = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - mn);
             m_run[qb] = mn;
             l_run[qb] *= alpha[qb];
         }
     }
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
         const float mb = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
         float ls = l_run[qb];
 #pragma unroll
@@ -324,16 +332,13 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[2][2], bf16x8 (&pf)[2][
     return resc;
 }
 
-template <int D, int SPAN>
-__global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint16_t* __restrict__ q,
-                                                         const uint16_t* __restrict__ k_pool,
-                                                         const uint16_t* __restrict__ v_pool,
-                                                         const int32_t* __restrict__ bt,
-                                                         float sm_scale, uint16_t* __restrict__ out,
-                                                         float* __restrict__ lse,
-                                                         float* __restrict__ part_o,
-                                                         float* __restrict__ part_lse) {
-    using G = Geo<D, SPAN>;
+template <int D, int SPAN, int QB>
+__global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
+    PlanData p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
+    const uint16_t* __restrict__ v_pool, const int32_t* __restrict__ bt, float sm_scale,
+    uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_o,
+    float* __restrict__ part_lse) {
+    using G = Geo<D, SPAN, QB>;
     __shared__ __attribute__((aligned(1024))) char smem[kStages * G::STAGE_BYTES];
 
     const WorkItem w = decode_item(p, blockIdx.x);
@@ -353,7 +358,7 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
     c.page_shift = p.page_shift;
     c.ps = p.page_size;
 
-    Loader<D, SPAN> ld;
+    Loader<D, SPAN, QB> ld;
     ld.init(wave, lane, c.ps);
 
     const int tb = w.tile_begin, te = w.tile_end;
@@ -367,11 +372,11 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
 
     // Query rows of this lane: one per 32-row block.
     const int rows_used = p.tile_tokens * Gq;
-    int qtok[2], qhead[2], qpos[2];
-    bf16x8 qf[2][G::KS];
+    int qtok[QB], qhead[QB], qpos[QB];
+    bf16x8 qf[QB][D / 16];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const int r = wave * 64 + qb * 32 + lq;
+    for (int qb = 0; qb < QB; ++qb) {
+        const int r = (wave * QB + qb) * 32 + lq;
         const int t = r / Gq;
         const bool valid = r < rows_used && t < w.num_tokens;
         qtok[qb] = valid ? t : -1;
@@ -380,41 +385,45 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
         const uint16_t* src = q + ((int64_t)(s.tok_off + w.first_token + t) * p.num_q_heads +
                                    qhead[qb]) * D + lh * 8;
 #pragma unroll
-        for (int ks = 0; ks < G::KS; ++ks) {
+        for (int ks = 0; ks < D / 16; ++ks) {
             u32x4 x = valid ? *reinterpret_cast<const u32x4*>(src + ks * 16) : u32x4{0, 0, 0, 0};
             qf[qb][ks] = __builtin_bit_cast(bf16x8, x);
         }
     }
 
     const float scale = sm_scale * kLog2e;  // logits in base-2 units
-    f32x16 o[2][G::DB];
+    f32x16 o[QB][D / 32];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-        for (int db = 0; db < G::DB; ++db)
+        for (int db = 0; db < D / 32; ++db)
             o[qb][db] = f32x16{};
-    float m_run[2] = {-INFINITY, -INFINITY};
-    float l_run[2] = {0.f, 0.f};   // this lane's partial row sums
-    float alpha[2] = {1.f, 1.f};
+    float m_run[QB], l_run[QB], alpha[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        m_run[qb] = -INFINITY;
+        l_run[qb] = 0.f;  // this lane's partial row sum
+        alpha[qb] = 1.f;
+    }
     bool resc = false;
 
     wait_vmem_all();
     __syncthreads();
     if (tb < te)
-        zero_v_tail<D, SPAN>(stage_ptr(tb), tb * kKeysPerTile, c.kv_len);
+        zero_v_tail<D, SPAN, QB>(stage_ptr(tb), tb * kKeysPerTile, c.kv_len);
     if (tb + 1 < te)
-        zero_v_tail<D, SPAN>(stage_ptr(tb + 1), (tb + 1) * kKeysPerTile, c.kv_len);
+        zero_v_tail<D, SPAN, QB>(stage_ptr(tb + 1), (tb + 1) * kKeysPerTile, c.kv_len);
     if (tb + 2 < te)
         ld.issue(stage_ptr(tb + 2), (tb + 2) * kKeysPerTile, c);
 
-    f32x16 sc[2][2];
-    bf16x8 pf[2][4];
+    f32x16 sc[QB][2];
+    bf16x8 pf[QB][4];
     if (tb < te)
-        qk_tile<D, SPAN>(sc, stage_ptr(tb), qf, lq, lh);
+        qk_tile<D, SPAN, QB>(sc, stage_ptr(tb), qf, lq, lh);
 
-    // First tile whose keys can lie past some row of the tile (needs the mask).
+    // tmask = smallest t with t * 64 + 63 > tile_first_pos (first tile that
+    // can hold keys past some row of the query tile).
     const int tile_first_pos = s.prefix_len + w.first_token;
-    // tmask = smallest t with t * 64 + 63 > tile_first_pos.
     const int tmask = tile_first_pos < kKeysPerTile - 1
                           ? 0 : (tile_first_pos - (kKeysPerTile - 1)) / kKeysPerTile + 1;
 
@@ -422,22 +431,23 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
         constexpr bool MASK = decltype(mask_tag)::value;
         if (resc) {  // rescale decided on S(t-1): before P(t-1) is accumulated
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-                for (int db = 0; db < G::DB; ++db)
+                for (int db = 0; db < D / 32; ++db)
                     o[qb][db] *= alpha[qb];
         }
         if (t > tb)
-            pv_tile<D, SPAN>(o, stage_ptr(t - 1), pf, lq, lh);
-        resc = softmax_tile<MASK>(sc, pf, m_run, l_run, alpha, scale, t * kKeysPerTile, qpos, lh);
+            pv_tile<D, SPAN, QB>(o, stage_ptr(t - 1), pf, lq, lh);
+        resc = softmax_tile<QB, MASK>(sc, pf, m_run, l_run, alpha, scale, t * kKeysPerTile, qpos,
+                                      lh);
         if (t + 1 < te)
-            qk_tile<D, SPAN>(sc, stage_ptr(t + 1), qf, lq, lh);
+            qk_tile<D, SPAN, QB>(sc, stage_ptr(t + 1), qf, lq, lh);
         wait_vmem_all();
         __syncthreads();
         if (t + 3 < te)
             ld.issue(stage_ptr(t + 3), (t + 3) * kKeysPerTile, c);
         if (t + 2 < te)
-            zero_v_tail<D, SPAN>(stage_ptr(t + 2), (t + 2) * kKeysPerTile, c.kv_len);
+            zero_v_tail<D, SPAN, QB>(stage_ptr(t + 2), (t + 2) * kKeysPerTile, c.kv_len);
     };
 
     const int split = tmask < tb ? tb : (tmask > te ? te : tmask);
@@ -449,29 +459,29 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
     if (tb < te) {
         if (resc) {
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-                for (int db = 0; db < G::DB; ++db)
+                for (int db = 0; db < D / 32; ++db)
                     o[qb][db] *= alpha[qb];
         }
-        pv_tile<D, SPAN>(o, stage_ptr(te - 1), pf, lq, lh);
+        pv_tile<D, SPAN, QB>(o, stage_ptr(te - 1), pf, lq, lh);
     }
 
     // Epilogue: full row sums, normalise, write.
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
         const float l = xhalf_sum(l_run[qb]);
         const float inv = l > 0.f ? 1.f / l : 0.f;
         const float lse2 = l > 0.f ? m_run[qb] + __log2f(l) : -INFINITY;
         if (qtok[qb] < 0)
             continue;
-        const int r = wave * 64 + qb * 32 + lq;
+        const int r = (wave * QB + qb) * 32 + lq;
         if (w.part_index < 0) {
             const int64_t row = (int64_t)(s.tok_off + w.first_token + qtok[qb]) * p.num_q_heads +
                                 qhead[qb];
             uint16_t* dst = out + row * D;
 #pragma unroll
-            for (int db = 0; db < G::DB; ++db)
+            for (int db = 0; db < D / 32; ++db)
 #pragma unroll
                 for (int j4 = 0; j4 < 4; ++j4) {
                     bf16x4 v;
@@ -485,7 +495,7 @@ __global__ __launch_bounds__(256, 1) void prefill_kernel(PlanData p, const uint1
         } else {
             float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D;
 #pragma unroll
-            for (int db = 0; db < G::DB; ++db)
+            for (int db = 0; db < D / 32; ++db)
 #pragma unroll
                 for (int j4 = 0; j4 < 4; ++j4) {
                     f32x4 v;
@@ -546,12 +556,16 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
         lse[row] = (mx + __log2f(wsum)) * kLn2;
 }
 
+// Rows per wave: 32 (8 waves, two per SIMD).
+constexpr int kQB = 1;
+
 template <int D, int SPAN>
 void launch_prefill_kernel(const PlanData& p, const uint16_t* q, const uint16_t* kp,
                            const uint16_t* vp, const int32_t* bt, float sm_scale, uint16_t* out,
                            float* lse, float* part_o, float* part_lse, hipStream_t st) {
-    hipLaunchKernelGGL((prefill_kernel<D, SPAN>), dim3(p.num_items), dim3(256), 0, st, p, q, kp,
-                       vp, bt, sm_scale, out, lse, part_o, part_lse);
+    hipLaunchKernelGGL((prefill_kernel<D, SPAN, kQB>), dim3(p.num_items),
+                       dim3(Geo<D, SPAN, kQB>::NT), 0, st, p, q, kp, vp, bt, sm_scale, out, lse,
+                       part_o, part_lse);
 }
 
 template <int D>

@@ -41,6 +41,7 @@
 #include <hip/hip_runtime.h>
 
 #include <math.h>
+#include <string.h>
 
 #include "common.h"
 
@@ -60,7 +61,7 @@ typedef __attribute__((address_space(1))) const void gbl_void;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
-constexpr int kStages = 4;
+constexpr int kStages = 5;
 
 struct NoMask {
     static constexpr bool value = false;
@@ -113,7 +114,7 @@ __device__ __forceinline__ float xhalf_max(float x) {
     // Lanes l and l^32 hold the two halves of one query row's keys.
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
                                                     false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float xhalf_sum(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
@@ -157,34 +158,53 @@ struct Loader {
         }
     }
 
-    // Issue the direct-to-LDS loads of the key tile starting at k0 into `stage`.
-    __device__ __forceinline__ void issue(char* stage, int k0, const Ctx& c) const {
+    // First key of K wave-load i / V wave-load i of a tile starting at k0.
+    __device__ __forceinline__ int kkey(int k0, int i) const {
+        return k0 + (wave * G::LOADS + i) * G::K_RPL;
+    }
+    __device__ __forceinline__ int vkey(int k0, int i) const {
+        return k0 + ((wave * G::LOADS + i) / G::V_LPB) * SPAN;
+    }
+
+    // Page ids of this wave's loads for the tile at k0 (scalar loads).  A
+    // load whose first key is past the end fetches from the sequence's last
+    // page instead: its contents land only at keys that are masked (K) or
+    // zeroed afterwards (V), and the page is owned by the sequence.
+    struct Pages {
+        int32_t k[G::LOADS];
+        int32_t v[G::LOADS];
+    };
+    __device__ __forceinline__ Pages pages(int k0, const Ctx& c) const {
+        Pages pg;
+        const int last = (c.kv_len - 1) >> c.page_shift;
+#pragma unroll
+        for (int i = 0; i < G::LOADS; ++i) {
+            pg.k[i] = c.bt_row[min(kkey(k0, i) >> c.page_shift, last)];
+            pg.v[i] = c.bt_row[min(vkey(k0, i) >> c.page_shift, last)];
+        }
+        return pg;
+    }
+
+    // Issue the direct-to-LDS loads of the tile at k0 into `stage`.
+    __device__ __forceinline__ void issue(char* stage, int k0, const Pages& pg,
+                                          const Ctx& c) const {
 #pragma unroll
         for (int i = 0; i < G::LOADS; ++i) {
             const int li = wave * G::LOADS + i;
-            const int key0 = k0 + li * G::K_RPL;
-            if (key0 < c.kv_len) {
-                const int64_t page = c.bt_row[key0 >> c.page_shift];
-                const char* src = c.kpool_g + page * c.page_bytes +
-                                  (int64_t)(key0 & (c.ps - 1)) * (D * 2) + koff[i];
-                __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)(stage + li * 1024),
-                                                 16, 0, 0);
-            }
+            const char* src = c.kpool_g + (int64_t)pg.k[i] * c.page_bytes +
+                              (int64_t)(kkey(k0, i) & (c.ps - 1)) * (D * 2) + koff[i];
+            __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)(stage + li * 1024), 16,
+                                             0, 0);
         }
 #pragma unroll
         for (int i = 0; i < G::LOADS; ++i) {
             const int li = wave * G::LOADS + i;
-            const int pj = li / G::V_LPB;
             const int bl = li % G::V_LPB;
-            const int key0 = k0 + pj * SPAN;
-            if (key0 < c.kv_len) {
-                const int64_t page = c.bt_row[key0 >> c.page_shift];
-                const char* src = c.vpool_g + page * c.page_bytes +
-                                  (int64_t)(bl * G::V_RPL) * c.ps * 2 +
-                                  (int64_t)(key0 & (c.ps - 1)) * 2 + voff[i];
-                __builtin_amdgcn_global_load_lds(
-                    (gbl_void*)src, (lds_void*)(stage + G::TILE_BYTES + li * 1024), 16, 0, 0);
-            }
+            const char* src = c.vpool_g + (int64_t)pg.v[i] * c.page_bytes +
+                              (int64_t)(bl * G::V_RPL) * c.ps * 2 +
+                              (int64_t)(vkey(k0, i) & (c.ps - 1)) * 2 + voff[i];
+            __builtin_amdgcn_global_load_lds(
+                (gbl_void*)src, (lds_void*)(stage + G::TILE_BYTES + li * 1024), 16, 0, 0);
         }
     }
 };
@@ -257,8 +277,10 @@ __device__ __forceinline__ void pv_tile(f32x16 (&o)[QB][D / 32], const char* sta
     }
 }
 
+// NaN-propagating maximum: gfx950 v_maximum3_f32 on MFMA results with no
+// quieting step (no score is NaN: masked scores are -inf before the max).
 __device__ __forceinline__ float max3f(float a, float b, float c) {
-    return __builtin_fmaxf(a, __builtin_fmaxf(b, c));
+    return __builtin_elementwise_maximum(a, __builtin_elementwise_maximum(b, c));
 }
 
 // One online-softmax step on S(t): returns P(t) as bf16 B-operands, updates
@@ -293,7 +315,7 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB
 #pragma unroll
         for (int j = 1; j < 15; j += 2)
             m = max3f(m, s[qb][1][j], s[qb][1][j + 1]);
-        m = __builtin_fmaxf(m, s[qb][1][15]);
+        m = __builtin_elementwise_maximum(m, s[qb][1][15]);
         mt[qb] = xhalf_max(m) * scale;
         grow = grow || (mt[qb] > m_run[qb] + kRescaleThreshold);
     }
@@ -362,13 +384,18 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     ld.init(wave, lane, c.ps);
 
     const int tb = w.tile_begin, te = w.tile_end;
-    auto stage_ptr = [&](int t) -> char* { return smem + (t & (kStages - 1)) * G::STAGE_BYTES; };
+    auto stage_ptr = [&](int t) -> char* { return smem + (t % kStages) * G::STAGE_BYTES; };
 
-    // Prologue loads: tiles tb, tb+1 (tile tb+2 is issued after the first wait).
-    if (tb < te)
-        ld.issue(stage_ptr(tb), tb * kKeysPerTile, c);
-    if (tb + 1 < te)
-        ld.issue(stage_ptr(tb + 1), (tb + 1) * kKeysPerTile, c);
+    // Prologue loads: tiles tb .. tb+2 (tile t+3 is issued at barrier t, with
+    // page ids fetched one barrier earlier).
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        if (tb + k < te)
+            ld.issue(stage_ptr(tb + k), (tb + k) * kKeysPerTile,
+                     ld.pages((tb + k) * kKeysPerTile, c), c);
+    typename Loader<D, SPAN, QB>::Pages pg_next;
+    if (tb + 3 < te)
+        pg_next = ld.pages((tb + 3) * kKeysPerTile, c);
 
     // Query rows of this lane: one per 32-row block.
     const int rows_used = p.tile_tokens * Gq;
@@ -407,17 +434,26 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     }
     bool resc = false;
 
+    {
+        // V of the stage that PV(tb-1) reads: zero, so 0 * V stays 0.
+        u32x4* vz = reinterpret_cast<u32x4*>(stage_ptr(tb - 1 + kStages) + G::TILE_BYTES);
+        for (int i = threadIdx.x; i < G::TILE_BYTES / 16; i += G::NT)
+            vz[i] = u32x4{0, 0, 0, 0};
+    }
     wait_vmem_all();
     __syncthreads();
-    if (tb < te)
-        zero_v_tail<D, SPAN, QB>(stage_ptr(tb), tb * kKeysPerTile, c.kv_len);
-    if (tb + 1 < te)
-        zero_v_tail<D, SPAN, QB>(stage_ptr(tb + 1), (tb + 1) * kKeysPerTile, c.kv_len);
-    if (tb + 2 < te)
-        ld.issue(stage_ptr(tb + 2), (tb + 2) * kKeysPerTile, c);
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+        if (tb + k < te)
+            zero_v_tail<D, SPAN, QB>(stage_ptr(tb + k), (tb + k) * kKeysPerTile, c.kv_len);
 
     f32x16 sc[QB][2];
     bf16x8 pf[QB][4];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            pf[qb][k] = bf16x8{};
     if (tb < te)
         qk_tile<D, SPAN, QB>(sc, stage_ptr(tb), qf, lq, lh);
 
@@ -427,27 +463,58 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     const int tmask = tile_first_pos < kKeysPerTile - 1
                           ? 0 : (tile_first_pos - (kKeysPerTile - 1)) / kKeysPerTile + 1;
 
+    // Ping-pong.  Every wave runs the same iteration -- softmax(t), then the
+    // MFMA phase PV(t-1) + QK(t+1) -- and passes one workgroup barrier per
+    // tile.  Waves of group B (the second wave on each SIMD) take that
+    // barrier between their two phases, group A after both, so B trails A by
+    // one phase: one wave's softmax runs while the other wave's MFMAs run.
+    // Between barriers t-1 and t the waves read V(t-2), V(t-1), K(t), K(t+1);
+    // loads of tile t+2 are in flight, hence five LDS stages.
+    // Invariant at the start of iteration t: sc = S(t), pf = P(t-1); a pending
+    // rescale (resc, alpha) from softmax(t-1) is applied to O just before
+    // P(t-1) is accumulated.
+    const bool group_b = wave >= G::NW / 2;
+    auto sync_point = [&](int t) {
+        wait_vmem_all();
+        __syncthreads();
+        if (t + 3 < te) {
+            ld.issue(stage_ptr(t + 3), (t + 3) * kKeysPerTile, pg_next, c);
+            if (t + 4 < te)
+                pg_next = ld.pages((t + 4) * kKeysPerTile, c);
+        }
+        if (t + 2 < te)
+            zero_v_tail<D, SPAN, QB>(stage_ptr(t + 2), (t + 2) * kKeysPerTile, c.kv_len);
+    };
     auto iteration = [&](int t, auto mask_tag) {
         constexpr bool MASK = decltype(mask_tag)::value;
-        if (resc) {  // rescale decided on S(t-1): before P(t-1) is accumulated
+        bf16x8 pn[QB][4];
+        float an[QB];
+        const bool rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile,
+                                               qpos, lh);
+        if (group_b)
+            sync_point(t);
+        __builtin_amdgcn_sched_barrier(0);
+        if (resc) {
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
                 for (int db = 0; db < D / 32; ++db)
                     o[qb][db] *= alpha[qb];
         }
-        if (t > tb)
-            pv_tile<D, SPAN, QB>(o, stage_ptr(t - 1), pf, lq, lh);
-        resc = softmax_tile<QB, MASK>(sc, pf, m_run, l_run, alpha, scale, t * kKeysPerTile, qpos,
-                                      lh);
-        if (t + 1 < te)
-            qk_tile<D, SPAN, QB>(sc, stage_ptr(t + 1), qf, lq, lh);
-        wait_vmem_all();
-        __syncthreads();
-        if (t + 3 < te)
-            ld.issue(stage_ptr(t + 3), (t + 3) * kKeysPerTile, c);
-        if (t + 2 < te)
-            zero_v_tail<D, SPAN, QB>(stage_ptr(t + 2), (t + 2) * kKeysPerTile, c.kv_len);
+        // MFMA phase, unconditional: P(tb-1) = 0 over a zeroed V stage, and
+        // S(te) comes from a stale stage and is never used.
+        pv_tile<D, SPAN, QB>(o, stage_ptr(t - 1 + kStages), pf, lq, lh);
+        qk_tile<D, SPAN, QB>(sc, stage_ptr(t + 1), qf, lq, lh);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                pf[qb][k] = pn[qb][k];
+            alpha[qb] = an[qb];
+        }
+        resc = rn;
+        if (!group_b)
+            sync_point(t);
     };
 
     const int split = tmask < tb ? tb : (tmask > te ? te : tmask);
@@ -616,7 +683,9 @@ extern "C" int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const void* 
     if (!q || !k_pool || !v_pool || !block_tables || !out)
         return fail(TALARIA_SP_EINVAL, "prefill: q, k_pool, v_pool, block_tables and out must "
                     "not be NULL");
-    if (!(sm_scale == sm_scale) || isinf(sm_scale))
+    uint32_t scale_bits;
+    memcpy(&scale_bits, &sm_scale, sizeof scale_bits);
+    if ((scale_bits & 0x7f800000u) == 0x7f800000u)
         return fail(TALARIA_SP_EINVAL, "prefill: sm_scale must be finite");
     if (sm_scale <= 0.f)
         sm_scale = 1.f / sqrtf((float)p->head_dim);

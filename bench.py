@@ -46,6 +46,9 @@ def parse():
                     help="write per-kernel / per-config figures to this file")
     ap.add_argument("--all-configs", action="store_true",
                     help="with --extra-json: also time every other config")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB three times "
+                         "(reference for the HBM traffic counters) and exit")
     return ap.parse_args()
 
 
@@ -195,6 +198,16 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n,
+                          "copies": 3}), flush=True)
+        return
     import paper_2607_17181_amd as tsa
     import gpu_harness as harness
     import workload

@@ -3,19 +3,19 @@
 // pool through the block tables (the batched prefill of an SP step, paper
 // Section 3.3, over the device-resident prefix of Section 4.3).
 //
-// One workgroup (4 waves, 256 threads) runs one work item of the plan: a
-// query tile of 256 rows -- tile_tokens new tokens times the `group` query
-// heads that share one KV head, so every K/V byte staged in LDS serves all of
-// them -- against one contiguous range of 64-key tiles.  Each wave owns 64
-// rows as two 32-row MFMA blocks; every K and V operand read from LDS feeds
-// both blocks.
+// One workgroup (8 waves, 512 threads, two waves per SIMD) runs one work item
+// of the plan: a query tile of 256 rows -- tile_tokens new tokens times the
+// `group` query heads that share one KV head, so every K/V byte staged in
+// LDS serves all of them -- against one contiguous range of 64-key tiles.
+// Each wave owns one 32-row MFMA block.
 //
 // Data movement.  K/V tiles move HBM -> LDS with global_load_lds_dwordx4
-// (no register staging), four tiles deep: each 1 KB wave-load stays inside
-// one page, so its page id is a wave-uniform scalar load of the block table
-// and the per-lane part of the address is loop-invariant.  Keys at or past
-// P_b + S_b are never fetched from unowned pages; V entries past the end are
-// zeroed in LDS so stale slots (even NaN) cannot reach the output.
+// (no register staging) into two rings, K four tiles deep and V five: all
+// of a wave's loads of one tile stay inside one page, so its page id is one
+// wave-uniform block-table load and the per-lane part of each address is
+// loop-invariant.  Keys at or past P_b + S_b are never fetched from unowned
+// pages; V entries past the end are zeroed in LDS so stale slots (even NaN)
+// cannot reach the output.
 //   K tile in LDS: 64 keys x D, natural key order, 16-byte chunks XOR-swizzled
 //                  by row.
 //   V tile in LDS: per page, [D][span] (tokens innermost, as in the pool),
@@ -27,11 +27,12 @@
 // no transpose.
 //
 // Pipeline (per wave, one iteration per key tile t):
-//     O   += V(t-1)^T P(t-1)      32 x v_mfma_f32_32x32x16_bf16
 //     P(t) = softmax step on S(t)  VALU: max, permlane32 swap, fma, exp2,
 //                                  cvt_pk_bf16, fp32 row sums
-//     S(t+1) = K(t+1) Q^T          32 x MFMA
-// The softmax of one tile runs between the MFMAs of its neighbours.  The
+//     O   += V(t-1)^T P(t-1)      D/8 x v_mfma_f32_32x32x16_bf16
+//     S(t+1) = K(t+1) Q^T          D/8 x MFMA
+// The two waves of a SIMD are one phase apart, so one wave's softmax runs
+// while the other's MFMAs do.  The
 // running maximum is lazy: O and l are rescaled only when some row's maximum
 // grows by more than 2^8, so exp2 arguments stay <= 8.
 //
@@ -61,7 +62,8 @@ typedef __attribute__((address_space(1))) const void gbl_void;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
-constexpr int kStages = 5;
+constexpr int kKStages = 4;  // K tile ring depth
+constexpr int kVStages = 5;  // V tile ring depth
 
 struct NoMask {
     static constexpr bool value = false;
@@ -75,7 +77,6 @@ struct Geo {
     static constexpr int NW = kRowsPerTile / (32 * QB);      // waves per workgroup
     static constexpr int NT = 64 * NW;                       // threads per workgroup
     static constexpr int TILE_BYTES = kKeysPerTile * D * 2;  // one K (or V) tile
-    static constexpr int STAGE_BYTES = 2 * TILE_BYTES;
     static constexpr int LOADS = TILE_BYTES / 1024 / NW;     // wave-loads per wave per tile
     static constexpr int K_CH = D / 8;                       // 16-byte chunks per K row
     static constexpr int K_RPL = 1024 / (2 * D);             // K rows per wave-load
@@ -125,6 +126,12 @@ __device__ __forceinline__ float xhalf_sum(float x) {
 __device__ __forceinline__ void wait_vmem_all() {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
+// Wait until at most N vector-memory loads of this wave are outstanding
+// (loads complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmem_n() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 struct Ctx {
     const char* kpool_g;      // K pool + head offset (bytes)
@@ -136,10 +143,16 @@ struct Ctx {
     int ps;
 };
 
+// Direct-to-LDS tile loads of one wave.  Wave w's K wave-loads cover tile
+// keys 8w .. 8w+7 and its V wave-loads cover the page block holding key 8w,
+// so for every supported page size (>= 8) all of a wave's loads of one tile
+// fall in the single page that holds key k0 + 8w: one block-table lookup
+// and one base address per wave and tile; the per-lane parts are
+// loop-invariant.
 template <int D, int SPAN, int QB>
 struct Loader {
     using G = Geo<D, SPAN, QB>;
-    uint32_t koff[G::LOADS];  // per-lane byte offsets (loop-invariant)
+    uint32_t koff[G::LOADS];  // per-lane byte offsets inside the page
     uint32_t voff[G::LOADS];
     int wave;
 
@@ -148,76 +161,55 @@ struct Loader {
 #pragma unroll
         for (int i = 0; i < G::LOADS; ++i) {
             const int li = w * G::LOADS + i;
-            const int row = li * G::K_RPL + lane / G::K_CH;
+            const int row0 = li * G::K_RPL;  // first tile key of the wave-load
+            const int row = row0 + lane / G::K_CH;
             const int lc = (lane % G::K_CH) ^ kswz<D>(row);
-            koff[i] = (uint32_t)(((lane / G::K_CH) * D + lc * 8) * 2);
+            koff[i] = (uint32_t)((((row0 & (ps - 1)) + lane / G::K_CH) * D + lc * 8) * 2);
             const int bl = li % G::V_LPB;
             const int d = bl * G::V_RPL + lane / G::V_CH;
             const int vlc = (lane % G::V_CH) ^ vswz<SPAN>(d);
-            voff[i] = (uint32_t)(((lane / G::V_CH) * ps + vlc * 8) * 2);
+            voff[i] = (uint32_t)(((bl * G::V_RPL + lane / G::V_CH) * ps + vlc * 8) * 2);
         }
     }
 
-    // First key of K wave-load i / V wave-load i of a tile starting at k0.
-    __device__ __forceinline__ int kkey(int k0, int i) const {
-        return k0 + (wave * G::LOADS + i) * G::K_RPL;
-    }
-    __device__ __forceinline__ int vkey(int k0, int i) const {
-        return k0 + ((wave * G::LOADS + i) / G::V_LPB) * SPAN;
-    }
-
-    // Page ids of this wave's loads for the tile at k0 (scalar loads).  A
-    // load whose first key is past the end fetches from the sequence's last
-    // page instead: its contents land only at keys that are masked (K) or
-    // zeroed afterwards (V), and the page is owned by the sequence.
-    struct Pages {
-        int32_t k[G::LOADS];
-        int32_t v[G::LOADS];
-    };
-    __device__ __forceinline__ Pages pages(int k0, const Ctx& c) const {
-        Pages pg;
-        const int last = (c.kv_len - 1) >> c.page_shift;
-#pragma unroll
-        for (int i = 0; i < G::LOADS; ++i) {
-            pg.k[i] = c.bt_row[min(kkey(k0, i) >> c.page_shift, last)];
-            pg.v[i] = c.bt_row[min(vkey(k0, i) >> c.page_shift, last)];
-        }
-        return pg;
+    // Block-table index of this wave's page for the tile at k0, clamped to
+    // the sequence's last page (a tile past the end then reads keys that are
+    // masked (K) or zeroed afterwards (V), from a page the sequence owns).
+    __device__ __forceinline__ int page_index(int k0, const Ctx& c) const {
+        return min((k0 + 8 * wave) >> c.page_shift, (c.kv_len - 1) >> c.page_shift);
     }
 
-    // Issue the direct-to-LDS loads of the tile at k0 into `stage`.
-    __device__ __forceinline__ void issue(char* stage, int k0, const Pages& pg,
-                                          const Ctx& c) const {
+    __device__ __forceinline__ void issue_k(char* buf, int k0, int32_t page,
+                                            const Ctx& c) const {
+        const char* base = c.kpool_g + (int64_t)page * c.page_bytes +
+                           (int64_t)(k0 & (c.ps - 1)) * (D * 2);
 #pragma unroll
-        for (int i = 0; i < G::LOADS; ++i) {
-            const int li = wave * G::LOADS + i;
-            const char* src = c.kpool_g + (int64_t)pg.k[i] * c.page_bytes +
-                              (int64_t)(kkey(k0, i) & (c.ps - 1)) * (D * 2) + koff[i];
-            __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)(stage + li * 1024), 16,
+        for (int i = 0; i < G::LOADS; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void*)(base + koff[i]),
+                                             (lds_void*)(buf + (wave * G::LOADS + i) * 1024), 16,
                                              0, 0);
-        }
+    }
+    __device__ __forceinline__ void issue_v(char* buf, int k0, int32_t page,
+                                            const Ctx& c) const {
+        const char* base = c.vpool_g + (int64_t)page * c.page_bytes +
+                           (int64_t)(k0 & (c.ps - 1)) * 2;
 #pragma unroll
-        for (int i = 0; i < G::LOADS; ++i) {
-            const int li = wave * G::LOADS + i;
-            const int bl = li % G::V_LPB;
-            const char* src = c.vpool_g + (int64_t)pg.v[i] * c.page_bytes +
-                              (int64_t)(bl * G::V_RPL) * c.ps * 2 +
-                              (int64_t)(vkey(k0, i) & (c.ps - 1)) * 2 + voff[i];
-            __builtin_amdgcn_global_load_lds(
-                (gbl_void*)src, (lds_void*)(stage + G::TILE_BYTES + li * 1024), 16, 0, 0);
-        }
+        for (int i = 0; i < G::LOADS; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void*)(base + voff[i]),
+                                             (lds_void*)(buf + (wave * G::LOADS + i) * 1024), 16,
+                                             0, 0);
     }
 };
 
-// Zero the V entries of keys kv_len .. k0+63 of the tile in `stage`.
+// Zero the V entries of keys kv_len .. k0+63 of the V tile in `vbuf`.
 template <int D, int SPAN, int QB>
-__device__ __forceinline__ void zero_v_tail(char* stage, int k0, int kv_len) {
+__device__ __forceinline__ void zero_v_tail(char* vbuf, int k0, int kv_len) {
     using G = Geo<D, SPAN, QB>;
     const int first = kv_len - k0;  // first key (tile-relative) past the end
     if (first >= kKeysPerTile)
         return;
     const int ntail = kKeysPerTile - first;
-    uint16_t* v = reinterpret_cast<uint16_t*>(stage + G::TILE_BYTES);
+    uint16_t* v = reinterpret_cast<uint16_t*>(vbuf);
     for (int e = threadIdx.x; e < D * ntail; e += G::NT) {
         const int d = e / ntail;
         const int key = first + e % ntail;
@@ -229,7 +221,7 @@ __device__ __forceinline__ void zero_v_tail(char* stage, int k0, int kv_len) {
 
 // S^T = K Q^T for the wave's QB 32-row blocks.
 template <int D, int SPAN, int QB>
-__device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* stage,
+__device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* kbuf,
                                         const bf16x8 (&qf)[QB][D / 16], int lq, int lh) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
@@ -243,7 +235,7 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* stage,
             const int row = kb * 32 + pi_row(lq);
             const int lc = 2 * ks + lh;
             const u32x4 a = *reinterpret_cast<const u32x4*>(
-                stage + row * (2 * D) + ((lc ^ kswz<D>(row)) << 4));
+                kbuf + row * (2 * D) + ((lc ^ kswz<D>(row)) << 4));
             const bf16x8 af = __builtin_bit_cast(bf16x8, a);
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb)
@@ -255,10 +247,9 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* stage,
 
 // O^T += V^T P^T for the wave's QB 32-row blocks.
 template <int D, int SPAN, int QB>
-__device__ __forceinline__ void pv_tile(f32x16 (&o)[QB][D / 32], const char* stage,
+__device__ __forceinline__ void pv_tile(f32x16 (&o)[QB][D / 32], const char* vt,
                                         const bf16x8 (&pf)[QB][4], int lq, int lh) {
     using G = Geo<D, SPAN, QB>;
-    const char* vt = stage + G::TILE_BYTES;
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
         const int key = 16 * ks2 + 8 * lh;
@@ -361,7 +352,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_o,
     float* __restrict__ part_lse) {
     using G = Geo<D, SPAN, QB>;
-    __shared__ __attribute__((aligned(1024))) char smem[kStages * G::STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) char smem[(kKStages + kVStages) * G::TILE_BYTES];
 
     const WorkItem w = decode_item(p, blockIdx.x);
     const SeqDesc s = p.seq[w.seq];
@@ -384,18 +375,33 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     ld.init(wave, lane, c.ps);
 
     const int tb = w.tile_begin, te = w.tile_end;
-    auto stage_ptr = [&](int t) -> char* { return smem + (t % kStages) * G::STAGE_BYTES; };
+    // Ring slots: K tile t in kbuf(t), V tile t in vbuf(t).
+    auto kbuf = [&](int t) -> char* { return smem + (t % kKStages) * G::TILE_BYTES; };
+    auto vbuf = [&](int t) -> char* {
+        return smem + (kKStages + t % kVStages) * G::TILE_BYTES;
+    };
 
-    // Prologue loads: tiles tb .. tb+2 (tile t+3 is issued at barrier t, with
-    // page ids fetched one barrier earlier).
+    // Load schedule.  In iteration t every wave issues its share of
+    // K(t + kd) and V(t + vd) from inside its MFMA phase, kd = 3 / vd = 2 for
+    // group A and kd = 4 / vd = 3 for group B (group A's MFMA phase precedes
+    // barrier t, group B's follows it), so in both groups the loads issued
+    // between barriers b-1 and b are K(b+4)/V(b+3)'s.  The prologue loads the
+    // tiles the first iterations need.  Loads are unconditional: a tile past
+    // the end reads the sequence's last page into a ring slot nobody reads.
+    const bool group_b = wave >= G::NW / 2;
+    const int kd = group_b ? 4 : 3, vd = group_b ? 3 : 2;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        if (k < kd)
+            ld.issue_k(kbuf(tb + k), (tb + k) * kKeysPerTile,
+                       c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
 #pragma unroll
     for (int k = 0; k < 3; ++k)
-        if (tb + k < te)
-            ld.issue(stage_ptr(tb + k), (tb + k) * kKeysPerTile,
-                     ld.pages((tb + k) * kKeysPerTile, c), c);
-    typename Loader<D, SPAN, QB>::Pages pg_next;
-    if (tb + 3 < te)
-        pg_next = ld.pages((tb + 3) * kKeysPerTile, c);
+        if (k < vd)
+            ld.issue_v(vbuf(tb + k), (tb + k) * kKeysPerTile,
+                       c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
+    int32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
+    int32_t pgv_next = c.bt_row[ld.page_index((tb + vd) * kKeysPerTile, c)];
 
     // Query rows of this lane: one per 32-row block.
     const int rows_used = p.tile_tokens * Gq;
@@ -435,8 +441,8 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     bool resc = false;
 
     {
-        // V of the stage that PV(tb-1) reads: zero, so 0 * V stays 0.
-        u32x4* vz = reinterpret_cast<u32x4*>(stage_ptr(tb - 1 + kStages) + G::TILE_BYTES);
+        // The V slot that PV(tb-1) reads: zero, so 0 * V stays 0.
+        u32x4* vz = reinterpret_cast<u32x4*>(vbuf(tb - 1 + kVStages));
         for (int i = threadIdx.x; i < G::TILE_BYTES / 16; i += G::NT)
             vz[i] = u32x4{0, 0, 0, 0};
     }
@@ -445,7 +451,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
 #pragma unroll
     for (int k = 0; k < 2; ++k)
         if (tb + k < te)
-            zero_v_tail<D, SPAN, QB>(stage_ptr(tb + k), (tb + k) * kKeysPerTile, c.kv_len);
+            zero_v_tail<D, SPAN, QB>(vbuf(tb + k), (tb + k) * kKeysPerTile, c.kv_len);
 
     f32x16 sc[QB][2];
     bf16x8 pf[QB][4];
@@ -455,7 +461,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         for (int k = 0; k < 4; ++k)
             pf[qb][k] = bf16x8{};
     if (tb < te)
-        qk_tile<D, SPAN, QB>(sc, stage_ptr(tb), qf, lq, lh);
+        qk_tile<D, SPAN, QB>(sc, kbuf(tb), qf, lq, lh);
 
     // tmask = smallest t with t * 64 + 63 > tile_first_pos (first tile that
     // can hold keys past some row of the query tile).
@@ -468,22 +474,19 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     // tile.  Waves of group B (the second wave on each SIMD) take that
     // barrier between their two phases, group A after both, so B trails A by
     // one phase: one wave's softmax runs while the other wave's MFMAs run.
-    // Between barriers t-1 and t the waves read V(t-2), V(t-1), K(t), K(t+1);
-    // loads of tile t+2 are in flight, hence five LDS stages.
+    // Between barriers t-1 and t the waves read K(t), K(t+1), V(t-2) and
+    // V(t-1); K(j) occupies its ring slot from barrier j-4 to j, V(j) from
+    // barrier j-3 to j+2.  A barrier waits only for the loads issued before
+    // the previous barrier (the 2 * LOADS issued since may stay in flight).
     // Invariant at the start of iteration t: sc = S(t), pf = P(t-1); a pending
     // rescale (resc, alpha) from softmax(t-1) is applied to O just before
     // P(t-1) is accumulated.
-    const bool group_b = wave >= G::NW / 2;
     auto sync_point = [&](int t) {
-        wait_vmem_all();
+        wait_vmem_n<2 * G::LOADS>();
         __syncthreads();
-        if (t + 3 < te) {
-            ld.issue(stage_ptr(t + 3), (t + 3) * kKeysPerTile, pg_next, c);
-            if (t + 4 < te)
-                pg_next = ld.pages((t + 4) * kKeysPerTile, c);
-        }
-        if (t + 2 < te)
-            zero_v_tail<D, SPAN, QB>(stage_ptr(t + 2), (t + 2) * kKeysPerTile, c.kv_len);
+        // V(t+1) landed before this barrier: clear its keys past the end.
+        if (t + 1 >= tb + 2 && t + 1 < te)
+            zero_v_tail<D, SPAN, QB>(vbuf(t + 1), (t + 1) * kKeysPerTile, c.kv_len);
     };
     auto iteration = [&](int t, auto mask_tag) {
         constexpr bool MASK = decltype(mask_tag)::value;
@@ -502,9 +505,13 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
                     o[qb][db] *= alpha[qb];
         }
         // MFMA phase, unconditional: P(tb-1) = 0 over a zeroed V stage, and
-        // S(te) comes from a stale stage and is never used.
-        pv_tile<D, SPAN, QB>(o, stage_ptr(t - 1 + kStages), pf, lq, lh);
-        qk_tile<D, SPAN, QB>(sc, stage_ptr(t + 1), qf, lq, lh);
+        // S(te) comes from a stale slot and is never used.
+        pv_tile<D, SPAN, QB>(o, vbuf(t - 1 + kVStages), pf, lq, lh);
+        ld.issue_k(kbuf(t + kd), (t + kd) * kKeysPerTile, pgk_next, c);
+        ld.issue_v(vbuf(t + vd), (t + vd) * kKeysPerTile, pgv_next, c);
+        qk_tile<D, SPAN, QB>(sc, kbuf(t + 1), qf, lq, lh);
+        pgk_next = c.bt_row[ld.page_index((t + 1 + kd) * kKeysPerTile, c)];
+        pgv_next = c.bt_row[ld.page_index((t + 1 + vd) * kKeysPerTile, c)];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
@@ -531,7 +538,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
                 for (int db = 0; db < D / 32; ++db)
                     o[qb][db] *= alpha[qb];
         }
-        pv_tile<D, SPAN, QB>(o, stage_ptr(te - 1), pf, lq, lh);
+        pv_tile<D, SPAN, QB>(o, vbuf(te - 1), pf, lq, lh);
     }
 
     // Epilogue: full row sums, normalise, write.

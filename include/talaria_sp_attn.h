@@ -2,7 +2,7 @@
  * talaria_sp_attn -- session-prefill (SP) attention over a paged KV pool on
  * one AMD Instinct MI355X (gfx950).
  *
- * The operation.  SP admission (paper Section 3.3, cold-pool scheduling)
+ * The operation.  SP admission (paper Section 3.4, cold-pool scheduling)
  * batch-prefills continuations of agent sessions whose prefix KV is already
  * resident on the device; only the new tail is computed (Section 4.3, Host KV
  * Registry: restore the agreed prefix into device slots, recompute only the
@@ -33,7 +33,7 @@
  *   k_pool      [num_pages][Hkv][page_size][head_dim]
  *   v_pool      [num_pages][Hkv][head_dim][page_size]   (token index innermost)
  *   block_tables[num_seqs][max_pages_per_seq] int32 (device memory)
- * One pool pair holds one layer ("layer-first" device layout, Appendix C).
+ * One pool pair holds one layer (layer-first device layout, Appendix C).
  * V pages keep tokens innermost so that the PV contraction, which reduces
  * over tokens, reads its operands contiguously.
  *
@@ -136,7 +136,7 @@ TALARIA_SP_API int talaria_sp_attn_append_kv(const talaria_sp_plan* plan, const 
 /*
  * Prefill: causal attention of every new token over its sequence's cached
  * prefix plus the new tokens (the batched prefill T_pf of an SP step,
- * Section 3.3), reading K/V through the block tables.  append_kv for the
+ * Section 3.4), reading K/V through the block tables.  append_kv for the
  * same plan must have been enqueued first.  Pool slots past P_b + S_b in a
  * sequence's last page, and block-table entries past its last page, are
  * never read, so stale contents there (even NaN) do not matter.

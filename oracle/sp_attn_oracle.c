@@ -7,9 +7,10 @@
  * fusion or online rescaling):
  *
  *   SP admission prefills a continuation whose prefix KV is already on the
- *   device, recomputing only the new tail (Sections 3.3 and 4.3 of the paper:
- *   "batched prefill" of the admitted set; restore the agreed prefix, then
- *   recompute only the unconfirmed tail into newly allocated device slots).
+ *   device, recomputing only the new tail (Sections 3.4 and 4.3 of the paper:
+ *   the admitted continuations are prefilled together as one batch; the
+ *   shared prefix is already in device pages and only the tokens after it
+ *   are computed, their KV going to fresh device pages).
  *   Sequence b has P_b cached tokens and S_b new tokens.  New token i sits
  *   at absolute position P_b + i and attends to keys 0 .. P_b + i
  *   (bottom-right causal alignment).  Query head h reads KV head
@@ -19,7 +20,7 @@
  *       lse  = ln sum_j exp(s_j)
  *   Logical position t of sequence b is stored in the page pool at page
  *   block_tables[b][t / page_size], slot t mod page_size (the paged device
- *   KV layout that HKVR restores into, Appendix C, "layer-first" view:
+ *   KV layout that HKVR restores into, Appendix C, layer-first view:
  *   one layer's pool, pages within the layer).  Within a page the K pool is
  *   [Hkv][page_size][d] and the V pool [Hkv][d][page_size]:
  *       K(t, g, e) = k_pool[((page * Hkv + g) * page_size + slot) * d + e]

@@ -1,7 +1,7 @@
 // Host planner for SP attention: argument validation, ragged offsets, and
 // the split of every query tile's key range into work items.
 //
-// The planner follows the shape of an SP step (Section 3.3): a bounded
+// The planner follows the shape of an SP step (Section 3.4): a bounded
 // batch of admitted continuations, each with its own committed prefix
 // length and new-token count.  It produces one flat work list that the
 // prefill kernel walks by block index:

@@ -1,7 +1,7 @@
 // SP prefill attention on gfx950: causal attention of each continuation's new
 // tokens over its cached prefix plus themselves, reading K/V from the paged
 // pool through the block tables (the batched prefill of an SP step, paper
-// Section 3.3, over the device-resident prefix of Section 4.3).
+// Section 3.4, over the device-resident prefix of Section 4.3).
 //
 // One workgroup (8 waves, 512 threads, two waves per SIMD) runs one work item
 // of the plan: a query tile of 256 rows -- tile_tokens new tokens times the

@@ -15,7 +15,7 @@ disagrees with:
 * a plain numpy scatter / concatenation for append and gather.
 
 The attention definition being pinned is the SP prefill of the paper's
-Sections 3.3 and 4.3 (prefill only the new tail of a continuation over its
+Sections 3.4 and 4.3 (prefill only the new tail of a continuation over its
 preserved prefix KV), with the causal alignment, head mapping and softmax
 scale readings stated in the oracle's header.
 """

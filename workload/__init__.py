@@ -6,7 +6,7 @@ sequence lengths, page permutations and block tables.  It contains none of
 the attention arithmetic, so the oracle and the HIP path can both consume
 its output without sharing any of the method's computation.
 
-Workload shapes follow the paper's trace statistics (Section 2, "Continuation
+Workload shapes follow the paper's trace statistics (Section 2.1, "Continuation
 inputs": median prompt 25K tokens, p95 105K) and the five synthetic
 configurations named in the module-level ``CONFIGS`` table.
 """

@@ -17,9 +17,12 @@ the suffixes need, so a sequence's pages are scattered over the whole pool
 and its suffix pages are not adjacent to its prefix pages.  Unused
 block-table entries hold -1.
 
-Nothing in this module computes attention or writes a page pool; the prefix
-is handed over as rows plus their flat slot indices, and the harness that
-owns a pool places them.
+Nothing in this module computes attention or appends to a pool.  The prefix
+is the cache state a continuation finds on the device, so it is input: it
+comes as rows plus their flat slot indices, and ``Workload.pool_bits`` lays
+those rows into fresh host pools (every other slot a sentinel) for the
+harnesses that want the resident state ready-made.  Appending the suffix, the
+method's own step, is left to each consumer.
 """
 from __future__ import annotations
 
@@ -31,7 +34,7 @@ import numpy as np
 
 BF16_NAN = np.uint16(0x7FC0)
 
-# Prompt-length statistics of the paper's agent trace (Section 2, "Continuation
+# Prompt-length statistics of the paper's agent trace (Section 2.1, "Continuation
 # inputs"): median 25K tokens, p95 105K.  The ragged config draws prefix
 # lengths from a lognormal with that median and p95, capped at 128K tokens.
 TRACE_MEDIAN_TOKENS = 25_000

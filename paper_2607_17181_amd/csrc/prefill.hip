@@ -604,18 +604,42 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
     const SeqDesc s = p.seq[w.seq];
     const int n = w.num_splits;
     const int sub = threadIdx.x % TPR;
+    const float* lse_k = part_lse + (int64_t)w.part_index * kRowsPerTile + r;
+    const float* o_k = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + sub * 4;
+    constexpr int64_t kStrideO = (int64_t)kRowsPerTile * D;
     float mx = -INFINITY;
-    for (int k = 0; k < n; ++k)
-        mx = fmaxf(mx, part_lse[(int64_t)(w.part_index + k) * kRowsPerTile + r]);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
-    for (int k = 0; k < n; ++k) {
-        const float lk = part_lse[(int64_t)(w.part_index + k) * kRowsPerTile + r];
-        const float wk = (lk == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk - mx);
-        wsum += wk;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(
-            part_o + ((int64_t)(w.part_index + k) * kRowsPerTile + r) * D + sub * 4);
-        acc += wk * v;
+    constexpr int KB = 8;  // splits whose loads are all issued up front
+    if (n <= KB) {
+        float lk[KB];
+        f32x4 v[KB];
+#pragma unroll
+        for (int k = 0; k < KB; ++k)
+            if (k < n) {
+                lk[k] = lse_k[k * kRowsPerTile];
+                v[k] = *reinterpret_cast<const f32x4*>(o_k + k * kStrideO);
+            }
+#pragma unroll
+        for (int k = 0; k < KB; ++k)
+            if (k < n)
+                mx = fmaxf(mx, lk[k]);
+#pragma unroll
+        for (int k = 0; k < KB; ++k)
+            if (k < n) {
+                const float wk = (lk[k] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk[k] - mx);
+                wsum += wk;
+                acc += wk * v[k];
+            }
+    } else {
+        for (int k = 0; k < n; ++k)
+            mx = fmaxf(mx, lse_k[k * kRowsPerTile]);
+        for (int k = 0; k < n; ++k) {
+            const float lk = lse_k[k * kRowsPerTile];
+            const float wk = (lk == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk - mx);
+            wsum += wk;
+            acc += wk * *reinterpret_cast<const f32x4*>(o_k + k * kStrideO);
+        }
     }
     const float inv = 1.f / wsum;
     const int t = r / G;

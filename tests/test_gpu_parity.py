@@ -146,6 +146,22 @@ def test_run_to_run_deterministic():
         assert np.array_equal(h.host_bits(db.run(plans=sp)[0]), first)
 
 
+def test_workspace_reuse_across_plans():
+    """One workspace serves plans of different split layouts in turn, and
+    outputs equal those of fresh workspaces bitwise (nothing in it carries
+    over from one call to the next)."""
+    h = _harness()
+    wl = SMALL["ragged_mixed"]()
+    db = h.DeviceBatch(wl)
+    plans = {k: db.plans(kv_splits=k) for k in (5, 3, 8)}
+    fresh = {k: h.host_bits(db.run(plans=p)[0]).copy() for k, p in plans.items()}
+    big = max(p[0].workspace_bytes for p in plans.values())
+    ws = torch.full((big,), 0x7F, dtype=torch.uint8, device="cuda")
+    for k in (5, 3, 8, 5, 3):
+        out = h.host_bits(db.run(plans=plans[k], workspaces=[ws])[0])
+        assert np.array_equal(out, fresh[k]), f"splits={k}"
+
+
 def test_split_count_invariance():
     h = _harness()
     wl, o_ref, _, _, _ = cached_oracle("gqa8_d128_unaligned")

@@ -152,6 +152,24 @@ def cpu_baseline(wl, rows_n, oracle, harness):
                       f"the same workload, fp64, {dt:.1f} s wall"}
 
 
+def measured_traffic(config):
+    """HBM bytes per prefill call from the committed counter summary, or None.
+
+    The summary records a hash of the kernel and planner sources it was taken
+    with; once those change the counters no longer describe the kernel and
+    the figure is withheld (None)."""
+    import hashlib
+    path = os.path.join(HERE, "profiles", f"prefill_{config}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    src = b"".join(open(os.path.join(HERE, s), "rb").read() for s in rec["sources"])
+    if hashlib.sha256(src).hexdigest() != rec["sources_sha256"]:
+        return None
+    return int(rec["traffic_bytes_per_call"])
+
+
 def standalone_bandwidth(torch, tsa, harness, workload, reps=20):
     """Append and gather GB/s on inputs larger than the 256 MB Infinity Cache."""
     res = {}
@@ -253,7 +271,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "prefill_kernel + combine_kernel (one prefill call)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic(args.config)},
     }
     extra = {"main": r}
     if args.extra_json:

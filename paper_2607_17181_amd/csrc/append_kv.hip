@@ -11,7 +11,9 @@
 // sequence, KV head).  K rows move as 16-byte chunks (page rows are
 // contiguous in both layouts).  V pages are stored tokens-innermost, so each
 // thread assembles 8 consecutive slots of one feature row and writes them
-// with one 16-byte store when the whole group lies inside the suffix.
+// with one 16-byte store when the whole group lies inside the suffix.  The
+// new rows are read once, so their loads are non-temporal; the pool stores
+// stay cached for the prefill that follows.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -53,7 +55,7 @@ __global__ __launch_bounds__(256) void append_kv_kernel(PlanData p, const uint16
         const u32x4* src = reinterpret_cast<const u32x4*>(k_new + (row * hkv + g) * D) + col;
         u32x4* dst = reinterpret_cast<u32x4*>(
                          k_pool + ((page * hkv + g) * ps + (pos & (ps - 1))) * D) + col;
-        *dst = *src;
+        *dst = __builtin_nontemporal_load(src);
     }
 
     // V: page block [D][ps]; groups of 8 slots of one feature row.
@@ -74,7 +76,7 @@ __global__ __launch_bounds__(256) void append_kv_kernel(PlanData p, const uint16
             } u;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                u.h[e] = v_new[((row0 + s0 + e) * hkv + g) * D + d];
+                u.h[e] = __builtin_nontemporal_load(v_new + ((row0 + s0 + e) * hkv + g) * D + d);
             *reinterpret_cast<u32x4*>(dst) = u.v;
         } else {
             for (int e = 0; e < 8; ++e) {

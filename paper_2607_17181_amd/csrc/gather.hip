@@ -12,6 +12,8 @@
 // tokens-innermost, so each thread reads 8 slots of one feature row with
 // one 16-byte load and scatters them to 8 output rows (a wave covers 64
 // consecutive features of one token per store, so stores stay coalesced).
+// Pool and output bytes stream through once: K copies and V loads are
+// non-temporal.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -47,7 +49,7 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(PlanData p, const uint16
         const u32x4* src = reinterpret_cast<const u32x4*>(
                                k_pool + ((page * hkv + g) * ps + sl) * D) + col;
         u32x4* dst = reinterpret_cast<u32x4*>(k_out + ((out0 + sl) * hkv + g) * D) + col;
-        *dst = *src;
+        __builtin_nontemporal_store(__builtin_nontemporal_load(src), dst);
     }
 
     const uint16_t* vpage = v_pool + (page * hkv + g) * (int64_t)D * ps;
@@ -59,7 +61,7 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(PlanData p, const uint16
             u32x4 v;
             uint16_t h[8];
         } u;
-        u.v = *reinterpret_cast<const u32x4*>(vpage + (int64_t)d * ps + s0);
+        u.v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vpage + (int64_t)d * ps + s0));
 #pragma unroll
         for (int e = 0; e < 8; ++e)
             if (s0 + e < ntok)

@@ -46,6 +46,9 @@ def parse():
                     help="write per-kernel / per-config figures to this file")
     ap.add_argument("--all-configs", action="store_true",
                     help="with --extra-json: also time every other config")
+    ap.add_argument("--hbm-sweep", action="store_true",
+                    help="only time append_kv / gather_kv on 0.1-2 GB batches (cache flushed) "
+                         "and print one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times "
                          "(reference for the HBM traffic counters) and exit")
@@ -170,40 +173,54 @@ def measured_traffic(config):
     return int(rec["traffic_bytes_per_call"])
 
 
-def standalone_bandwidth(torch, tsa, harness, workload, reps=20):
-    """Append and gather GB/s on inputs larger than the 256 MB Infinity Cache."""
-    res = {}
-    for name in ("cold", "ragged"):
-        wl = workload.make_workload(name)
-        db = harness.DeviceBatch(wl, fill=0)
-        sp = db.plans()[0]
-        # append
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt)
+def hbm_sweep(torch, tsa, reps=10):
+    """append_kv / gather_kv GB/s on synthetic batches of 102 MB to 2 GB, with
+    the 256 MB Infinity Cache flushed (1 GiB written) before every repetition."""
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+
+    def timeit(fn):
+        fn()
         torch.cuda.synchronize()
-        t0.record()
-        for _ in range(reps):
-            tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt)
-        t1.record()
-        torch.cuda.synchronize()
-        ms = t0.elapsed_time(t1) / reps
-        nbytes = 2 * 2 * wl.total_tokens * wl.num_kv_heads * wl.head_dim * 2
-        res[f"append_{name}"] = {"ms": ms, "bytes": nbytes, "gbs": nbytes / ms / 1e6}
-        # gather
-        n = sp.total_kv_tokens
-        ko = torch.empty((n, wl.num_kv_heads, wl.head_dim), dtype=torch.int16, device="cuda")
+        ts = []
+        for r in range(reps):
+            scratch.fill_(r)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    res = []
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    for nseq, S, P in [(4, 25_000, 0), (16, 4_096, 25_000), (8, 250_000, 0)]:
+        hkv, d, ps = 1, 128, 16
+        pages = (P + S + ps - 1) // ps
+        num_pages = nseq * pages + 64
+        T = nseq * S
+        sp = tsa.plan(tsa.make_geom(8, hkv, d, ps, num_pages), [P] * nseq, [S] * nseq, pages)
+        perm = torch.randperm(num_pages, device="cuda", generator=gen, dtype=torch.int32)
+        bt = perm[: nseq * pages].view(nseq, pages).contiguous()
+        kp = torch.zeros((num_pages, hkv, ps, d), dtype=torch.int16, device="cuda")
+        vp = torch.zeros((num_pages, hkv, d, ps), dtype=torch.int16, device="cuda")
+        kn = torch.randint(-30000, 30000, (T, hkv, d), dtype=torch.int16, device="cuda",
+                           generator=gen)
+        vn = torch.randint(-30000, 30000, (T, hkv, d), dtype=torch.int16, device="cuda",
+                           generator=gen)
+        ms = timeit(lambda: tsa.append_kv(sp, kn, vn, kp, vp, bt))
+        nbytes = 2 * 2 * T * hkv * d * 2
+        res.append({"kernel": "append_kv", "batch": f"{nseq}x(P={P},S={S})", "bytes": nbytes,
+                    "us": round(ms * 1e3, 1), "gbs": round(nbytes / ms / 1e6)})
+        nk = nseq * (P + S)
+        ko = torch.empty((nk, hkv, d), dtype=torch.int16, device="cuda")
         vo = torch.empty_like(ko)
-        tsa.gather_kv(sp, db.k_pool, db.v_pool, db.bt, ko, vo)
-        torch.cuda.synchronize()
-        t0.record()
-        for _ in range(reps):
-            tsa.gather_kv(sp, db.k_pool, db.v_pool, db.bt, ko, vo)
-        t1.record()
-        torch.cuda.synchronize()
-        ms = t0.elapsed_time(t1) / reps
-        nbytes = 2 * 2 * n * wl.num_kv_heads * wl.head_dim * 2
-        res[f"gather_{name}"] = {"ms": ms, "bytes": nbytes, "gbs": nbytes / ms / 1e6}
-        del db, ko, vo
+        ms = timeit(lambda: tsa.gather_kv(sp, kp, vp, bt, ko, vo))
+        nbytes = 2 * 2 * nk * hkv * d * 2
+        res.append({"kernel": "gather_kv", "batch": f"{nseq}x(P={P},S={S})", "bytes": nbytes,
+                    "us": round(ms * 1e3, 1), "gbs": round(nbytes / ms / 1e6)})
+        del kp, vp, kn, vn, ko, vo
         torch.cuda.empty_cache()
     return res
 
@@ -234,6 +251,10 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.hbm_sweep:
+        print(json.dumps({"hbm_sweep": hbm_sweep(torch, tsa), "peak_gbs": PEAK_HBM_GBS}),
+              flush=True)
+        return
 
     r = time_config(args.config, args.steps, args.warmup, torch, tsa, harness, workload)
     wl = r.pop("wl")
@@ -275,7 +296,7 @@ def main():
     }
     extra = {"main": r}
     if args.extra_json:
-        extra["bandwidth"] = standalone_bandwidth(torch, tsa, harness, workload)
+        extra["hbm_sweep"] = hbm_sweep(torch, tsa)
         if args.all_configs:
             for name in ("tiny", "ragged", "long", "cold"):
                 if name == args.config:

@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--hbm-sweep", action="store_true",
                     help="only time append_kv / gather_kv on 0.1-2 GB batches (cache flushed) "
                          "and print one JSON line")
+    ap.add_argument("--hkvr", action="store_true",
+                    help="only time HKVR restore/checkpoint of a 25K-token prefix over 94 "
+                         "layers and print one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times "
                          "(reference for the HBM traffic counters) and exit")
@@ -225,6 +228,49 @@ def hbm_sweep(torch, tsa, reps=10):
     return res
 
 
+def hkvr_bench(torch, tsa, layers=94, prefix=25_000, reps=5):
+    """HKVR restore (host slab -> device pages) and checkpoint (device -> host)
+    of one continuation's page-aligned prefix across all layers of one TP
+    rank's share of a 94-layer GQA model (Hkv=1, d=128, page 16), against a
+    plain pinned-host <-> device copy of the same bytes."""
+    ps, d, hkv = 16, 128, 1
+    n = prefix // ps
+    num_pages = n + 1024
+    cache = tsa.kv_cache(layers, hkv, d, ps, num_pages)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7)
+    ids = torch.randperm(num_pages, device="cuda", generator=gen, dtype=torch.int32)[:n]
+    kc = torch.zeros((layers, num_pages, hkv, ps, d), dtype=torch.int16, device="cuda")
+    vc = torch.zeros((layers, num_pages, hkv, d, ps), dtype=torch.int16, device="cuda")
+    slab = torch.empty(tsa.slab_shape(cache, n), dtype=torch.int16, pin_memory=True)
+    slab.random_(-30000, 30000)
+    flat = torch.empty(slab.numel(), dtype=torch.int16, device="cuda")
+
+    def timeit(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    nbytes = slab.numel() * 2
+    out = {"workload": f"{layers} layers x {n} pages (P={n * ps}), Hkv={hkv} d={d} page {ps}",
+           "bytes": nbytes}
+    for name, fn in [("restore", lambda: tsa.hkvr_restore(cache, slab, ids, kc, vc)),
+                     ("checkpoint", lambda: tsa.hkvr_checkpoint(cache, kc, vc, ids, slab)),
+                     ("memcpy_h2d", lambda: flat.copy_(slab.view(-1), non_blocking=True)),
+                     ("memcpy_d2h", lambda: slab.view(-1).copy_(flat, non_blocking=True))]:
+        ms = timeit(fn)
+        out[name] = {"ms": round(ms, 3), "gbs": round(nbytes / ms / 1e6, 1)}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -251,6 +297,9 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.hkvr:
+        print(json.dumps({"hkvr": hkvr_bench(torch, tsa)}), flush=True)
+        return
     if args.hbm_sweep:
         print(json.dumps({"hbm_sweep": hbm_sweep(torch, tsa), "peak_gbs": PEAK_HBM_GBS}),
               flush=True)

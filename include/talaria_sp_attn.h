@@ -176,6 +176,54 @@ TALARIA_SP_API int talaria_sp_attn_gather_kv(const talaria_sp_plan* plan, const 
  * Returns the number of work items (>= 0) or a negative status. */
 TALARIA_SP_API int talaria_sp_attn_plan_items(const talaria_sp_plan* plan, int32_t* items, int32_t max_items);
 
+/* ---- HKVR page transfer (host KV registry restore / checkpoint) ----------
+ *
+ * A returning session's prefix may live in pinned host memory instead of the
+ * device cache.  Restoring it places the agreed prefix pages into newly
+ * allocated device pages before the unconfirmed tail is recomputed (Section
+ * 4.3); checkpointing copies device pages out when a turn ends.  The two
+ * layouts are the layer-first device cache and the page-first host slab of
+ * Appendix C:
+ *
+ *   k_cache  [num_layers][num_pages][Hkv][page_size][head_dim]   (device)
+ *   v_cache  [num_layers][num_pages][Hkv][head_dim][page_size]   (device)
+ *   slab     [num_slab_pages][num_layers][2][Hkv*page_size*head_dim] (host)
+ *
+ * Layer l of the cache is the single-layer pool pair the attention calls
+ * above take (k_cache + l * num_pages * Hkv * page_size * head_dim, and
+ * likewise for V).  Slab block [p][l][0] is device page page_ids[p] of layer
+ * l's K pool and [p][l][1] the same page of its V pool, each in the device
+ * page's own element order, so a transfer moves whole page blocks and
+ * reorders no element.  Whole pages only: restored prefixes are page
+ * aligned.
+ *
+ * The slab must be pinned host memory that the device can address directly
+ * (hipHostMalloc, or a torch tensor allocated with pin_memory=True); the
+ * copy kernels read or write it through that address over the host link.
+ * page_ids is a device int32 array of num_slab_pages entries (typically the
+ * first entries of the sequence's block-table row); an entry outside
+ * [0, num_pages) moves nothing.  Entries should be distinct: two slab pages
+ * naming one device page race on restore.  Stream-ordered like the calls
+ * above; nothing synchronises.
+ */
+typedef struct {
+    int32_t num_layers;    /* 1 .. 65535 */
+    int32_t num_kv_heads;
+    int32_t head_dim;      /* 64 or 128 */
+    int32_t page_size;     /* power of two in [8, 256] */
+    int32_t num_pages;     /* device pages per layer */
+} talaria_kv_cache;
+
+/* Host slab -> device cache (H2D restore of num_slab_pages pages, all layers). */
+TALARIA_SP_API int talaria_hkvr_restore(const talaria_kv_cache* cache, int32_t num_slab_pages,
+                                        const void* slab, const int32_t* page_ids,
+                                        void* k_cache, void* v_cache, void* stream);
+
+/* Device cache -> host slab (D2H checkpoint of num_slab_pages pages, all layers). */
+TALARIA_SP_API int talaria_hkvr_checkpoint(const talaria_kv_cache* cache, int32_t num_slab_pages,
+                                           const void* k_cache, const void* v_cache,
+                                           const int32_t* page_ids, void* slab, void* stream);
+
 /* Message for the last failing call on this thread ("" if none). */
 TALARIA_SP_API const char* talaria_sp_last_error(void);
 

@@ -9,6 +9,8 @@ The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
     sp = plan(geom, prefix_lens, suffix_lens, max_pages_per_seq)
     append_kv(sp, k_new, v_new, k_pool, v_pool, block_tables)
     prefill(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)
+    hkvr_restore(cache, slab, page_ids, k_cache, v_cache)       # host -> device pages
+    hkvr_checkpoint(cache, k_cache, v_cache, page_ids, slab)    # device pages -> host
 
 Device arrays are ``torch`` tensors (bf16 data may also be passed as int16
 or uint16 bit patterns); torch provides device memory and the current
@@ -48,6 +50,13 @@ class Geom(ctypes.Structure):
                 ("num_pages", ctypes.c_int32)]
 
 
+class KvCache(ctypes.Structure):
+    """Geometry of a layer-first device KV cache (talaria_kv_cache)."""
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32)]
+
+
 class _RawPlan(ctypes.Structure):
     _fields_ = [("opaque", ctypes.c_uint64 * PLAN_WORDS)]
 
@@ -75,6 +84,10 @@ def library() -> ctypes.CDLL:
                   lib.talaria_sp_attn_prefill, lib.talaria_sp_attn_gather_kv,
                   lib.talaria_sp_attn_plan_items):
             f.restype = ctypes.c_int
+        lib.talaria_hkvr_restore.argtypes = [ctypes.POINTER(KvCache), i32, p, p, p, p, p]
+        lib.talaria_hkvr_checkpoint.argtypes = [ctypes.POINTER(KvCache), i32, p, p, p, p, p]
+        lib.talaria_hkvr_restore.restype = ctypes.c_int
+        lib.talaria_hkvr_checkpoint.restype = ctypes.c_int
         lib.talaria_sp_last_error.argtypes = []
         lib.talaria_sp_last_error.restype = ctypes.c_char_p
         _lib = lib
@@ -244,3 +257,56 @@ def workspace_tensor(sp: SpPlan, device="cuda"):
     if sp.workspace_bytes == 0:
         return None
     return _torch().empty(sp.workspace_bytes, dtype=_torch().uint8, device=device)
+
+
+# ---- HKVR page transfer ---------------------------------------------------------------
+
+def kv_cache(num_layers: int, num_kv_heads: int, head_dim: int, page_size: int,
+             num_pages: int) -> KvCache:
+    return KvCache(num_layers, num_kv_heads, head_dim, page_size, num_pages)
+
+
+def _cache_shapes(c: KvCache):
+    k = (c.num_layers, c.num_pages, c.num_kv_heads, c.page_size, c.head_dim)
+    v = (c.num_layers, c.num_pages, c.num_kv_heads, c.head_dim, c.page_size)
+    return k, v
+
+
+def slab_shape(c: KvCache, num_slab_pages: int):
+    """Page-first host slab: [pages][layers][K, V][Hkv * page_size * head_dim]."""
+    return (num_slab_pages, c.num_layers, 2, c.num_kv_heads * c.page_size * c.head_dim)
+
+
+def _slab(t, shape):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or t.is_cuda or not t.is_pinned():
+        raise ValueError("slab must be a pinned host tensor (pin_memory=True)")
+    if t.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+        raise TypeError(f"slab must be bf16 (or 16-bit bit patterns), got {t.dtype}")
+    if not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"slab has shape {tuple(t.shape)}, expected contiguous {tuple(shape)}")
+    return t.data_ptr()
+
+
+def _hkvr_args(c, slab, page_ids, k_cache, v_cache):
+    torch = _torch()
+    kshape, vshape = _cache_shapes(c)
+    n = int(page_ids.shape[0]) if page_ids.dim() == 1 else -1
+    if n < 0:
+        raise ValueError("page_ids must be 1-D")
+    return n, (_slab(slab, slab_shape(c, n)),
+               _dev(page_ids, (n,), "page_ids", bits16=False, dtype=torch.int32),
+               _dev(k_cache, kshape, "k_cache"), _dev(v_cache, vshape, "v_cache"))
+
+
+def hkvr_restore(c: KvCache, slab, page_ids, k_cache, v_cache, stream=None) -> None:
+    """talaria_hkvr_restore: page-first host slab -> layer-first device pages."""
+    n, (sp, ip, kp, vp) = _hkvr_args(c, slab, page_ids, k_cache, v_cache)
+    _check(library().talaria_hkvr_restore(ctypes.byref(c), n, sp, ip, kp, vp, _stream(stream)))
+
+
+def hkvr_checkpoint(c: KvCache, k_cache, v_cache, page_ids, slab, stream=None) -> None:
+    """talaria_hkvr_checkpoint: layer-first device pages -> page-first host slab."""
+    n, (sp, ip, kp, vp) = _hkvr_args(c, slab, page_ids, k_cache, v_cache)
+    _check(library().talaria_hkvr_checkpoint(ctypes.byref(c), n, kp, vp, ip, sp,
+                                             _stream(stream)))

@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--hkvr", action="store_true",
                     help="only time HKVR restore/checkpoint of a 25K-token prefix over 94 "
                          "layers and print one JSON line")
+    ap.add_argument("--stage", action="store_true",
+                    help="only time the D2D-staged weight gather (4 GiB) and print one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times "
                          "(reference for the HBM traffic counters) and exit")
@@ -271,6 +273,60 @@ def hkvr_bench(torch, tsa, layers=94, prefix=25_000, reps=5):
     return out
 
 
+def stage_bench(torch, tsa, weight_gib=4, chunk_mib=2, reps=5):
+    """D2D-staged switch: assemble a weight region of weight_gib GiB from
+    chunk_mib MiB chunks, (a) all staged and clean (pure D2D), (b) with the
+    chunks under 10% of the KV pages dirty (D2D + H2D top-up), (c) all from
+    host (pure H2D); plus the dirty-marking kernel."""
+    chunk = chunk_mib << 20
+    n = (weight_gib << 30) // chunk
+    page = 64 << 10
+    stage_bytes = n * chunk + (64 << 20)
+    chunks = torch.tensor([[(64 << 20) + i * chunk, i * chunk, chunk] for i in range(n)],
+                          dtype=torch.int64, device="cuda")
+    staging = torch.zeros(stage_bytes, dtype=torch.uint8, device="cuda")
+    weights = torch.empty(n * chunk, dtype=torch.uint8, device="cuda")
+    host = torch.empty(n * chunk, dtype=torch.uint8, pin_memory=True)
+    num_pages = stage_bytes // page
+    words = (num_pages + 31) // 32
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(3)
+    used_bits = torch.rand(num_pages, device="cuda", generator=gen) < 0.001  # scattered KV pages
+    w = torch.zeros(words * 32, dtype=torch.int64, device="cuda")
+    w[:num_pages] = used_bits.to(torch.int64)
+    used = (w.view(words, 32) << torch.arange(32, device="cuda")).sum(1).to(torch.int32)
+    cw = (n + 31) // 32
+    all_set = torch.full((cw,), -1, dtype=torch.int32, device="cuda")
+    none_set = torch.zeros(cw, dtype=torch.int32, device="cuda")
+    dirty = torch.zeros(cw, dtype=torch.int32, device="cuda")
+
+    def timeit(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    ms_mark = timeit(lambda: tsa.stage_mark_dirty(chunks, used, num_pages, page, dirty))
+    n_dirty = int(sum(bin(int(x) & 0xFFFFFFFF).count("1") for x in dirty.cpu().tolist()))
+    nbytes = n * chunk
+    res = {"workload": f"{n} chunks x {chunk_mib} MiB = {nbytes / 2**30:.0f} GiB of weights",
+           "mark_dirty_us": round(ms_mark * 1e3, 1), "dirty_chunks": n_dirty}
+    for name, stg, drt in [("all_d2d", all_set, none_set), ("d2d_plus_h2d", all_set, dirty),
+                           ("all_h2d", none_set, none_set)]:
+        ms = timeit(lambda: tsa.stage_gather(chunks, stg, drt, staging, host, weights))
+        # weight bytes placed per second; a D2D chunk also reads as many HBM bytes
+        res[name] = {"ms": round(ms, 3), "weight_gbs": round(nbytes / ms / 1e6, 1)}
+    res["all_d2d"]["hbm_read_write_gbs"] = round(2 * nbytes / res["all_d2d"]["ms"] / 1e6, 1)
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -297,6 +353,9 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.stage:
+        print(json.dumps({"stage": stage_bench(torch, tsa)}), flush=True)
+        return
     if args.hkvr:
         print(json.dumps({"hkvr": hkvr_bench(torch, tsa)}), flush=True)
         return

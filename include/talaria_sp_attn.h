@@ -224,6 +224,49 @@ TALARIA_SP_API int talaria_hkvr_checkpoint(const talaria_kv_cache* cache, int32_
                                            const void* k_cache, const void* v_cache,
                                            const int32_t* page_ids, void* slab, void* stream);
 
+/* ---- D2D-staged weight switching (staging guard and gather) -------------
+ *
+ * The next model's weights are pre-staged in fixed-size chunks in unused
+ * high-address HBM of the KV region while the current model serves; at the
+ * switch, staged clean chunks are copied device to device and the rest is
+ * reloaded from host (Section 4.4).  A staged chunk becomes dirty when a KV
+ * allocation takes pages overlapping its staging range.
+ *
+ * Regions (byte addresses, 16-byte aligned):
+ *   staging       device, staging_bytes: the region the staged copies sit in;
+ *                 also the region whose pages the KV allocator hands out
+ *                 (page p = bytes [p*page_bytes, (p+1)*page_bytes)).
+ *   weights       device, weight_bytes: the target model's weight region.
+ *   host_weights  pinned host memory with the same layout as weights.
+ * Chunk i (talaria_stage_chunk, device array) moves `bytes` bytes to
+ * weights + weight_offset, from staging + stage_offset when bit i of `staged`
+ * is set and bit i of `dirty` is clear, else from host_weights +
+ * weight_offset.  Sizes and offsets are multiples of 16.  A chunk whose
+ * weight range leaves the weight region is skipped; a staged range outside
+ * the staging region falls back to the host copy.  Bitmaps are device
+ * uint32 arrays, bit i = word i/32, bit i%32.
+ */
+typedef struct {
+    int64_t stage_offset;   /* byte offset of the staged copy in `staging` */
+    int64_t weight_offset;  /* byte offset in `weights` (and `host_weights`) */
+    int64_t bytes;          /* chunk size, a positive multiple of 16 */
+} talaria_stage_chunk;
+
+/* dirty bit i = 1 iff some page p with bit p of used_pages set overlaps
+ * chunk i's staging range (pages >= num_pages are not tracked).  Writes all
+ * ceil(num_chunks/32) words of dirty. */
+TALARIA_SP_API int talaria_stage_mark_dirty(const talaria_stage_chunk* chunks, int32_t num_chunks,
+                                            const uint32_t* used_pages, int64_t num_pages,
+                                            int64_t page_bytes, uint32_t* dirty, void* stream);
+
+/* Assemble the weight region from clean staged chunks (D2D) and host copies
+ * (H2D) in one kernel. */
+TALARIA_SP_API int talaria_stage_gather(const talaria_stage_chunk* chunks, int32_t num_chunks,
+                                        const uint32_t* staged, const uint32_t* dirty,
+                                        const void* staging, int64_t staging_bytes,
+                                        const void* host_weights, void* weights,
+                                        int64_t weight_bytes, void* stream);
+
 /* Message for the last failing call on this thread ("" if none). */
 TALARIA_SP_API const char* talaria_sp_last_error(void);
 

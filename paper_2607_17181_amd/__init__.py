@@ -88,6 +88,11 @@ def library() -> ctypes.CDLL:
         lib.talaria_hkvr_checkpoint.argtypes = [ctypes.POINTER(KvCache), i32, p, p, p, p, p]
         lib.talaria_hkvr_restore.restype = ctypes.c_int
         lib.talaria_hkvr_checkpoint.restype = ctypes.c_int
+        i64 = ctypes.c_int64
+        lib.talaria_stage_mark_dirty.argtypes = [p, i32, p, i64, i64, p, p]
+        lib.talaria_stage_gather.argtypes = [p, i32, p, p, p, i64, p, p, i64, p]
+        lib.talaria_stage_mark_dirty.restype = ctypes.c_int
+        lib.talaria_stage_gather.restype = ctypes.c_int
         lib.talaria_sp_last_error.argtypes = []
         lib.talaria_sp_last_error.restype = ctypes.c_char_p
         _lib = lib
@@ -310,3 +315,45 @@ def hkvr_checkpoint(c: KvCache, k_cache, v_cache, page_ids, slab, stream=None) -
     n, (sp, ip, kp, vp) = _hkvr_args(c, slab, page_ids, k_cache, v_cache)
     _check(library().talaria_hkvr_checkpoint(ctypes.byref(c), n, kp, vp, ip, sp,
                                              _stream(stream)))
+
+
+# ---- D2D-staged weight switching ------------------------------------------------------
+
+def _words(n_bits: int) -> int:
+    return (n_bits + 31) // 32
+
+
+def _u8dev(t, what):
+    torch = _torch()
+    return _dev(t, None, what, bits16=False, dtype=torch.uint8)
+
+
+def stage_mark_dirty(chunks, used_pages, num_pages: int, page_bytes: int, dirty,
+                     stream=None) -> None:
+    """talaria_stage_mark_dirty.  chunks: device int64 [n, 3] (stage_offset,
+    weight_offset, bytes); used_pages / dirty: device int32 bitmaps."""
+    torch = _torch()
+    n = int(chunks.shape[0])
+    cp = _dev(chunks, (n, 3), "chunks", bits16=False, dtype=torch.int64)
+    up = _dev(used_pages, (_words(num_pages),), "used_pages", bits16=False, dtype=torch.int32)
+    dp = _dev(dirty, (_words(n),), "dirty", bits16=False, dtype=torch.int32)
+    _check(library().talaria_stage_mark_dirty(cp, n, up, int(num_pages), int(page_bytes), dp,
+                                              _stream(stream)))
+
+
+def stage_gather(chunks, staged, dirty, staging, host_weights, weights, stream=None) -> None:
+    """talaria_stage_gather.  staging / weights: device uint8; host_weights:
+    pinned host uint8 with the weights' size."""
+    torch = _torch()
+    n = int(chunks.shape[0])
+    cp = _dev(chunks, (n, 3), "chunks", bits16=False, dtype=torch.int64)
+    sp = _dev(staged, (_words(n),), "staged", bits16=False, dtype=torch.int32)
+    dp = _dev(dirty, (_words(n),), "dirty", bits16=False, dtype=torch.int32)
+    if host_weights.is_cuda or not host_weights.is_pinned() or host_weights.dtype != torch.uint8:
+        raise ValueError("host_weights must be a pinned host uint8 tensor")
+    if host_weights.numel() != weights.numel() or not host_weights.is_contiguous():
+        raise ValueError("host_weights must be contiguous with the weights' size")
+    _check(library().talaria_stage_gather(cp, n, sp, dp, _u8dev(staging, "staging"),
+                                          staging.numel(), host_weights.data_ptr(),
+                                          _u8dev(weights, "weights"), weights.numel(),
+                                          _stream(stream)))

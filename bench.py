@@ -54,6 +54,8 @@ def parse():
                          "layers and print one JSON line")
     ap.add_argument("--stage", action="store_true",
                     help="only time the D2D-staged weight gather (4 GiB) and print one JSON line")
+    ap.add_argument("--select", action="store_true",
+                    help="only time SP batch selection over 1000 candidates (host)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times "
                          "(reference for the HBM traffic counters) and exit")
@@ -327,6 +329,23 @@ def stage_bench(torch, tsa, weight_gib=4, chunk_mib=2, reps=5):
     return res
 
 
+def select_bench(tsa, n=1000, reps=200):
+    """Host latency of SP batch selection over n queued continuations."""
+    rng = np.random.default_rng(11)
+    cands = np.stack([np.minimum(np.round(np.exp(rng.normal(np.log(25_000), 0.87247, n))), 131_072),
+                      rng.integers(512, 4097, n), (rng.random(n) < 0.3)],
+                     axis=1).astype(np.int32)
+    model = tsa.CostModel(94, 8, 1, 128, 16, 1.0e15, 1e-5, 50e9, 1e-3)
+    budget = tsa.Budget(2.0, 200_000, 128)
+    tsa.sp_select(cands, model, budget)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        sel, *_ = tsa.sp_select(cands, model, budget)
+    us = (time.perf_counter() - t0) / reps * 1e6
+    return {"candidates": n, "admitted": int(len(sel)), "us_per_call": round(us, 2),
+            "note": "includes the Python binding's marshalling"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -334,6 +353,10 @@ def main():
               "sharded by KV head or by sequence with no exchange, see the design notes.",
               file=sys.stderr)
         sys.exit(2)
+    if args.select:
+        import paper_2607_17181_amd as tsa
+        print(json.dumps({"select": select_bench(tsa)}), flush=True)
+        return
     import torch
     if args.copy_calibration:
         n = args.copy_calibration << 20

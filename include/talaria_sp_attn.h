@@ -267,6 +267,59 @@ TALARIA_SP_API int talaria_stage_gather(const talaria_stage_chunk* chunks, int32
                                         const void* host_weights, void* weights,
                                         int64_t weight_bytes, void* stream);
 
+/* ---- SP batch selection (host) -------------------------------------------
+ *
+ * At an SP opportunity the scheduler admits a bounded batch of the eligible
+ * continuations whose predicted prefill, restore and HBM costs fit what the
+ * slot has left after protected decode; calls that do not fit stay queued
+ * (Section 3.4).  talaria_sp_select scans candidates in queue order and
+ * admits each one that still fits all bounds (first fit), skipping the rest.
+ *
+ * Predicted cost of a candidate (host-resident prefixes are restored page
+ * aligned, their partial last page recomputed with the suffix, Appendix B:
+ * P' = floor(P/ps)*ps, S' = S + P - P'; device-resident ones keep P, S):
+ *   seconds = 4*d*Hq*layers*(S*P + S*(S+1)/2) / attn_flops_per_s
+ *           + S * per_token_s
+ *           + (host-resident) (P/ps) * 2*Hkv*ps*d*2*layers bytes / restore_bytes_per_s
+ *   pages   = ceil((P+S)/ps) - (device-resident ? ceil(P/ps) : 0)
+ * plus batch_overhead_s once per non-empty batch.  Candidates with S <= 0
+ * or P < 0 are never admitted.
+ *
+ * selected          out: indices of admitted candidates, in queue order
+ *                   (room for max_batch entries)
+ * plan_prefix_lens, plan_suffix_lens
+ *                   out (may be NULL): the admitted candidates' P and S as
+ *                   talaria_sp_attn_plan takes them (after the alignment above)
+ * predicted_seconds, predicted_pages
+ *                   out (may be NULL): the batch's predicted totals
+ * Returns the number admitted (>= 0) or a negative status.  Host only.
+ */
+typedef struct {
+    int32_t prefix_len;     /* P: committed (device) or checkpointed (host) tokens */
+    int32_t suffix_len;     /* S: new tokens to prefill */
+    int32_t host_resident;  /* nonzero: the prefix must be restored from host */
+} talaria_sp_candidate;
+
+typedef struct {
+    int32_t num_layers, num_q_heads, num_kv_heads, head_dim, page_size;
+    double attn_flops_per_s;    /* sustained SP attention FLOP/s */
+    double per_token_s;         /* other prefill work per new token */
+    double restore_bytes_per_s; /* host -> device restore rate */
+    double batch_overhead_s;    /* fixed cost of one SP batch */
+} talaria_sp_cost_model;
+
+typedef struct {
+    double time_budget_s;   /* prefill + restore time left in the slot */
+    int64_t free_pages;     /* device pages the batch may allocate */
+    int32_t max_batch;      /* 0 .. TALARIA_SP_MAX_SEQS */
+} talaria_sp_budget;
+
+TALARIA_SP_API int talaria_sp_select(const talaria_sp_candidate* cands, int32_t num_cands,
+                                     const talaria_sp_cost_model* model,
+                                     const talaria_sp_budget* budget, int32_t* selected,
+                                     int32_t* plan_prefix_lens, int32_t* plan_suffix_lens,
+                                     double* predicted_seconds, int64_t* predicted_pages);
+
 /* Message for the last failing call on this thread ("" if none). */
 TALARIA_SP_API const char* talaria_sp_last_error(void);
 

@@ -57,6 +57,21 @@ class KvCache(ctypes.Structure):
                 ("num_pages", ctypes.c_int32)]
 
 
+class CostModel(ctypes.Structure):
+    """talaria_sp_cost_model: predicted-cost coefficients of SP selection."""
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("attn_flops_per_s", ctypes.c_double),
+                ("per_token_s", ctypes.c_double), ("restore_bytes_per_s", ctypes.c_double),
+                ("batch_overhead_s", ctypes.c_double)]
+
+
+class Budget(ctypes.Structure):
+    """talaria_sp_budget: what the slot has left after protected decode."""
+    _fields_ = [("time_budget_s", ctypes.c_double), ("free_pages", ctypes.c_int64),
+                ("max_batch", ctypes.c_int32)]
+
+
 class _RawPlan(ctypes.Structure):
     _fields_ = [("opaque", ctypes.c_uint64 * PLAN_WORDS)]
 
@@ -93,6 +108,11 @@ def library() -> ctypes.CDLL:
         lib.talaria_stage_gather.argtypes = [p, i32, p, p, p, i64, p, p, i64, p]
         lib.talaria_stage_mark_dirty.restype = ctypes.c_int
         lib.talaria_stage_gather.restype = ctypes.c_int
+        lib.talaria_sp_select.argtypes = [p, i32, ctypes.POINTER(CostModel),
+                                          ctypes.POINTER(Budget), p, p, p,
+                                          ctypes.POINTER(ctypes.c_double),
+                                          ctypes.POINTER(ctypes.c_int64)]
+        lib.talaria_sp_select.restype = ctypes.c_int
         lib.talaria_sp_last_error.argtypes = []
         lib.talaria_sp_last_error.restype = ctypes.c_char_p
         _lib = lib
@@ -357,3 +377,23 @@ def stage_gather(chunks, staged, dirty, staging, host_weights, weights, stream=N
                                           staging.numel(), host_weights.data_ptr(),
                                           _u8dev(weights, "weights"), weights.numel(),
                                           _stream(stream)))
+
+
+# ---- SP batch selection (host) --------------------------------------------------------
+
+def sp_select(candidates, model: CostModel, budget: Budget):
+    """talaria_sp_select.  candidates: int32 [n, 3] rows (prefix_len,
+    suffix_len, host_resident).  Returns (selected indices, plan prefix
+    lengths, plan suffix lengths, predicted seconds, predicted pages)."""
+    c = np.ascontiguousarray(candidates, dtype=np.int32).reshape(-1, 3)
+    cap = max(int(budget.max_batch), 1)
+    sel = np.zeros(cap, np.int32)
+    pre = np.zeros(cap, np.int32)
+    suf = np.zeros(cap, np.int32)
+    secs = ctypes.c_double(0.0)
+    pages = ctypes.c_int64(0)
+    n = _check(library().talaria_sp_select(
+        c.ctypes.data if c.size else None, c.shape[0], ctypes.byref(model), ctypes.byref(budget),
+        sel.ctypes.data, pre.ctypes.data, suf.ctypes.data, ctypes.byref(secs),
+        ctypes.byref(pages)))
+    return sel[:n].copy(), pre[:n].copy(), suf[:n].copy(), secs.value, pages.value

@@ -56,6 +56,8 @@ def parse():
                     help="only time the D2D-staged weight gather (4 GiB) and print one JSON line")
     ap.add_argument("--select", action="store_true",
                     help="only time SP batch selection over 1000 candidates (host)")
+    ap.add_argument("--decode", action="store_true",
+                    help="only time a 64-sequence decode step and print one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times "
                          "(reference for the HBM traffic counters) and exit")
@@ -346,6 +348,47 @@ def select_bench(tsa, n=1000, reps=200):
             "note": "includes the Python binding's marshalling"}
 
 
+def decode_bench(torch, tsa, harness, workload, n_seqs=64, reps=20):
+    """Decode step of a batch of continuations: lognormal contexts (median
+    25K, p95 105K tokens), one new token each, Hq=8 Hkv=1 d=128 page 16.
+    GB/s = K/V bytes of every context position read once / decode call time;
+    the same plan run through the prefill kernel for comparison."""
+    rng = np.random.default_rng(17)
+    pre = workload.lognormal_prefix_lengths(rng, n_seqs).tolist()
+    need = sum((p_ + 1 + 15) // 16 for p_ in pre)
+    wl = workload.workload_from_lengths("decode", 17, num_q_heads=8, num_kv_heads=1,
+                                        head_dim=128, page_size=16, num_pages=need + 1024,
+                                        prefix_lens=pre, suffix_lens=[1] * n_seqs)
+    db = harness.DeviceBatch(wl, fill=0)
+    sp = db.plans()[0]
+    ws = tsa.workspace_tensor(sp)
+    tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt)
+
+    def timeit(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    kv_bytes = int(sum(p_ + 1 for p_ in pre)) * wl.num_kv_heads * wl.head_dim * 2 * 2
+    ms_dec = timeit(lambda: tsa.decode(sp, db.q, db.k_pool, db.v_pool, db.bt, db.out, db.lse, ws))
+    ms_pre = timeit(lambda: tsa.prefill(sp, db.q, db.k_pool, db.v_pool, db.bt, db.out, db.lse, ws))
+    ms_app = timeit(lambda: tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt))
+    return {"workload": f"decode step of {n_seqs} continuations, contexts lognormal median 25K "
+                        f"(total {sum(pre) + n_seqs} positions), Hq=8 Hkv=1 d=128 page 16",
+            "items": int(tsa.plan_items(sp).shape[0]), "kv_bytes": kv_bytes,
+            "decode_call_us": round(ms_dec * 1e3, 1),
+            "decode_gbs": round(kv_bytes / ms_dec / 1e6, 1),
+            "prefill_path_us": round(ms_pre * 1e3, 1),
+            "prefill_path_gbs": round(kv_bytes / ms_pre / 1e6, 1),
+            "append_us": round(ms_app * 1e3, 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -376,6 +419,11 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.decode:
+        import gpu_harness as harness
+        import workload
+        print(json.dumps({"decode": decode_bench(torch, tsa, harness, workload)}), flush=True)
+        return
     if args.stage:
         print(json.dumps({"stage": stage_bench(torch, tsa)}), flush=True)
         return

@@ -159,6 +159,22 @@ TALARIA_SP_API int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const vo
                             void* stream);
 
 /*
+ * Decode: the S_b = 1 case of prefill -- each sequence's one new token (at
+ * position P_b, its K/V appended first) attends to keys 0 .. P_b -- with a
+ * kernel built for it: the D phase that resumes after an SP batch (Section
+ * 3.4) reads every cached K/V byte once for only `group` query rows, so it
+ * is bound by HBM, not by the matrix cores.  Same plan (made with suffix
+ * lengths of 0 or 1), arguments, layouts and workspace as prefill.
+ * EINVAL if some suffix length exceeds 1; EUNSUPPORTED if more than 32
+ * query heads share a KV head.
+ */
+TALARIA_SP_API int talaria_sp_attn_decode(const talaria_sp_plan* plan, const void* q,
+                                          const void* k_pool, const void* v_pool,
+                                          const int32_t* block_tables, float sm_scale, void* out,
+                                          float* lse, void* workspace, size_t workspace_bytes,
+                                          void* stream);
+
+/*
  * Gather: copy positions 0 .. P_b+S_b-1 of every sequence out of the pool
  * into contiguous token-major rows -- the block-table page walk that the
  * prefill kernel performs internally, as a standalone copy (the layer-first

@@ -94,6 +94,9 @@ def library() -> ctypes.CDLL:
         lib.talaria_sp_attn_prefill.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
                                                 ctypes.c_float, p, p, p, sz, p]
         lib.talaria_sp_attn_gather_kv.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p]
+        lib.talaria_sp_attn_decode.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
+                                               ctypes.c_float, p, p, p, sz, p]
+        lib.talaria_sp_attn_decode.restype = ctypes.c_int
         lib.talaria_sp_attn_plan_items.argtypes = [ctypes.POINTER(_RawPlan), p, i32]
         for f in (lib.talaria_sp_attn_plan, lib.talaria_sp_attn_append_kv,
                   lib.talaria_sp_attn_prefill, lib.talaria_sp_attn_gather_kv,
@@ -240,9 +243,8 @@ def append_kv(sp: SpPlan, k_new, v_new, k_pool, v_pool, block_tables, stream=Non
     _check(library().talaria_sp_attn_append_kv(ctypes.byref(sp.raw), *args, _stream(stream)))
 
 
-def prefill(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspace=None,
-            sm_scale: float = 0.0, stream=None) -> None:
-    """talaria_sp_attn_prefill: causal SP attention into ``out`` (and ``lse``)."""
+def _attention_call(fn, sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse, workspace,
+                    sm_scale, stream) -> None:
     torch = _torch()
     g = sp.geom
     kshape, vshape = _pool_shapes(sp)
@@ -259,9 +261,22 @@ def prefill(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspac
     args = (_dev(q, qshape, "q"), _dev(k_pool, kshape, "k_pool"), _dev(v_pool, vshape, "v_pool"),
             _dev(block_tables, (sp.num_seqs, sp.max_pages_per_seq), "block_tables",
                  bits16=False, dtype=torch.int32))
-    _check(library().talaria_sp_attn_prefill(ctypes.byref(sp.raw), *args, float(sm_scale),
-                                             _dev(out, qshape, "out"), lse_ptr, ws_ptr, ws_bytes,
-                                             _stream(stream)))
+    _check(fn(ctypes.byref(sp.raw), *args, float(sm_scale), _dev(out, qshape, "out"), lse_ptr,
+              ws_ptr, ws_bytes, _stream(stream)))
+
+
+def prefill(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspace=None,
+            sm_scale: float = 0.0, stream=None) -> None:
+    """talaria_sp_attn_prefill: causal SP attention into ``out`` (and ``lse``)."""
+    _attention_call(library().talaria_sp_attn_prefill, sp, q, k_pool, v_pool, block_tables, out,
+                    lse, workspace, sm_scale, stream)
+
+
+def decode(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspace=None,
+           sm_scale: float = 0.0, stream=None) -> None:
+    """talaria_sp_attn_decode: one new token per sequence (suffix lengths <= 1)."""
+    _attention_call(library().talaria_sp_attn_decode, sp, q, k_pool, v_pool, block_tables, out,
+                    lse, workspace, sm_scale, stream)
 
 
 def gather_kv(sp: SpPlan, k_pool, v_pool, block_tables, k_out, v_out, stream=None) -> None:

@@ -16,7 +16,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtalaria_sp_attn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["plan.cpp", "append_kv.hip", "gather.hip", "prefill.hip", "hkvr.hip", "stage.hip", "select.cpp"]
+SOURCES = ["plan.cpp", "append_kv.hip", "gather.hip", "prefill.hip", "hkvr.hip", "stage.hip", "select.cpp", "decode.hip"]
 
 # Per-source extra flags (none at present).
 EXTRA = {}

@@ -19,3 +19,17 @@ const PlanData* checked_plan(const talaria_sp_plan* plan, int* status);
 int launch_status(const char* what);
 
 }  // namespace tsp
+
+#if defined(__HIPCC__)
+#include <hip/hip_runtime.h>
+namespace tsp {
+// Merge the split partials of a plan into out / lse (no-op when nothing is
+// split).  Defined with the prefill kernel.
+int launch_combine(const PlanData& p, const float* part_o, const float* part_lse, uint16_t* out,
+                   float* lse, hipStream_t st);
+}  // namespace tsp
+#endif
+
+namespace tsp {
+
+}  // namespace tsp

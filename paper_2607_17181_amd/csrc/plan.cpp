@@ -34,6 +34,11 @@ thread_local char g_error[512] = "";
 constexpr int kConcurrentItems = 256;
 // Never cut a key range below this many key tiles.
 constexpr int kMinTilesPerSplit = 8;
+// Decode batches: two decode workgroups fit on a CU (LDS bound), so a decode
+// batch is cut for twice as many concurrent items; and the shortest key
+// range worth a split.
+constexpr int kDecodeItemsPerCU = 2;
+constexpr int kMinTilesPerDecodeSplit = 4;
 }  // namespace
 
 int fail(int code, const char* fmt, ...) {
@@ -160,10 +165,19 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     // Target key tiles per item: the per-CU share of the batch when the
     // batch alone cannot fill the GPU (one round of equal items), half of it
     // otherwise (so that a long sequence's items cannot form a long tail).
-    double share = total_cost / kConcurrentItems;
-    if (base_items >= kConcurrentItems)
+    //
+    // A decode batch (every suffix at most one token) streams K/V for very
+    // few query rows: its items are HBM-bound and cheap in compute, so it is
+    // cut kDecodeItemsPerCU times finer to keep every resident slot busy.
+    bool decode_batch = true;
+    for (int32_t b = 0; b < num_seqs; ++b)
+        decode_batch = decode_batch && suffix_lens[b] <= 1;
+    const int concurrent = decode_batch ? kDecodeItemsPerCU * kConcurrentItems : kConcurrentItems;
+    double share = total_cost / concurrent;
+    if (base_items >= concurrent)
         share *= 0.5;
-    const double target = std::max<double>(kMinTilesPerSplit, share);
+    const double target = std::max<double>(decode_batch ? kMinTilesPerDecodeSplit
+                                                        : kMinTilesPerSplit, share);
 
     int64_t items = 0, part_items = 0;
     for (int32_t b = 0; b < num_seqs; ++b) {

@@ -607,39 +607,41 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
     const float* lse_k = part_lse + (int64_t)w.part_index * kRowsPerTile + r;
     const float* o_k = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + sub * 4;
     constexpr int64_t kStrideO = (int64_t)kRowsPerTile * D;
+    // Online merge in split order, KB splits per round of loads (all issued
+    // before any is used): the running maximum only grows, and the sums are
+    // rescaled when it does.
     float mx = -INFINITY;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
-    constexpr int KB = 8;  // splits whose loads are all issued up front
-    if (n <= KB) {
+    constexpr int KB = 8;
+    for (int k0 = 0; k0 < n; k0 += KB) {
         float lk[KB];
         f32x4 v[KB];
 #pragma unroll
-        for (int k = 0; k < KB; ++k)
-            if (k < n) {
-                lk[k] = lse_k[k * kRowsPerTile];
-                v[k] = *reinterpret_cast<const f32x4*>(o_k + k * kStrideO);
+        for (int k = 0; k < KB; ++k) {
+            lk[k] = -INFINITY;
+            if (k0 + k < n) {
+                lk[k] = lse_k[(k0 + k) * kRowsPerTile];
+                v[k] = *reinterpret_cast<const f32x4*>(o_k + (k0 + k) * kStrideO);
             }
+        }
+        float cm = mx;
 #pragma unroll
         for (int k = 0; k < KB; ++k)
-            if (k < n)
-                mx = fmaxf(mx, lk[k]);
+            cm = fmaxf(cm, lk[k]);
+        if (cm > mx) {
+            const float a = __builtin_amdgcn_exp2f(mx - cm);  // 0 while mx is -inf
+            wsum *= a;
+            acc *= a;
+            mx = cm;
+        }
 #pragma unroll
         for (int k = 0; k < KB; ++k)
-            if (k < n) {
+            if (k0 + k < n) {
                 const float wk = (lk[k] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk[k] - mx);
                 wsum += wk;
                 acc += wk * v[k];
             }
-    } else {
-        for (int k = 0; k < n; ++k)
-            mx = fmaxf(mx, lse_k[k * kRowsPerTile]);
-        for (int k = 0; k < n; ++k) {
-            const float lk = lse_k[k * kRowsPerTile];
-            const float wk = (lk == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk - mx);
-            wsum += wk;
-            acc += wk * *reinterpret_cast<const f32x4*>(o_k + k * kStrideO);
-        }
     }
     const float inv = 1.f / wsum;
     const int t = r / G;
@@ -687,15 +689,40 @@ int launch_prefill(const PlanData& p, const uint16_t* q, const uint16_t* kp, con
         break;
     }
     int status = launch_status("prefill");
-    if (status != TALARIA_SP_OK || p.num_part_items == 0)
+    if (status != TALARIA_SP_OK)
         return status;
-    constexpr int RPB = 256 / (D / 4);
-    hipLaunchKernelGGL(combine_kernel<D>, dim3(p.num_items, kRowsPerTile / RPB), dim3(256), 0, st,
-                       p, part_o, part_lse, out, lse);
-    return launch_status("combine");
+    return launch_combine(p, part_o, part_lse, out, lse, st);
 }
 
 }  // namespace
+
+int launch_combine(const PlanData& p, const float* part_o, const float* part_lse, uint16_t* out,
+                   float* lse, hipStream_t st) {
+    if (p.num_part_items == 0)
+        return TALARIA_SP_OK;
+    // Rows of the tallest split query tile: the grid covers no more (a
+    // decode batch's split tiles hold `group` rows, not kRowsPerTile).
+    int32_t rows = 0;
+    for (int32_t b = 0; b < p.num_seqs; ++b)
+        if (num_splits_of(p, b) > 1) {
+            const int32_t t = p.seq[b].suffix_len < p.tile_tokens ? p.seq[b].suffix_len
+                                                                  : p.tile_tokens;
+            rows = rows > t * p.group ? rows : t * p.group;
+        }
+    if (rows == 0)
+        return TALARIA_SP_OK;
+    if (p.head_dim == 128) {
+        constexpr int RPB = 256 / (128 / 4);
+        hipLaunchKernelGGL(combine_kernel<128>, dim3(p.num_items, ceil_div(rows, RPB)), dim3(256),
+                           0, st, p, part_o, part_lse, out, lse);
+    } else {
+        constexpr int RPB = 256 / (64 / 4);
+        hipLaunchKernelGGL(combine_kernel<64>, dim3(p.num_items, ceil_div(rows, RPB)), dim3(256), 0,
+                           st, p, part_o, part_lse, out, lse);
+    }
+    return launch_status("combine");
+}
+
 }  // namespace tsp
 
 using namespace tsp;

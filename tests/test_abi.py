@@ -1,6 +1,7 @@
 """The C-ABI library on the CPU: it loads, exports every declared symbol, and
 its host planner covers every (query row, key) pair exactly once, balances
 work and rejects bad arguments without touching the device."""
+import ctypes
 import os
 import re
 
@@ -21,7 +22,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = tsa.library()
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     for n in names:
         assert hasattr(lib, n), n
 
@@ -167,3 +168,15 @@ def test_prefill_checks_arguments_before_launching():
     st = lib.talaria_sp_attn_prefill(sp.raw, fake, fake, fake, fake, float("nan"), fake, None,
                                      fake, sp.workspace_bytes, None)
     assert st == tsa.EINVAL
+
+
+def test_decode_rejects_multi_token_plans_without_launching():
+    sp = tsa.plan(_geom(), [100, 5], [1, 2], 16)
+    fake = 0x1000
+    rc = tsa.library().talaria_sp_attn_decode(ctypes.byref(sp.raw), fake, fake, fake, fake, 0.0,
+                                              fake, None, None, 0, None)
+    assert rc == tsa.EINVAL and "new tokens" in tsa.last_error()
+    sp = tsa.plan(tsa.make_geom(64, 1, 128, 16, 1000), [100], [1], 16)
+    rc = tsa.library().talaria_sp_attn_decode(ctypes.byref(sp.raw), fake, fake, fake, fake, 0.0,
+                                              fake, None, None, 0, None)
+    assert rc == tsa.EUNSUPPORTED

@@ -46,7 +46,7 @@ def _decode(wl, splits):
     return h, h.host_bits(db.out), db.lse.cpu().numpy()
 
 
-@pytest.mark.parametrize("splits", [0, 1, 3])
+@pytest.mark.parametrize("splits", [0, 1, 3, 20])
 @pytest.mark.parametrize("name", list(CASES))
 def test_decode_matches_oracle(name, splits):
     wl = _wl(name)

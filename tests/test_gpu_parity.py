@@ -79,6 +79,20 @@ def test_prefill_matches_oracle(name, splits):
     assert lse_err <= h.LSE_ABS, f"lse error {lse_err}"
 
 
+@pytest.mark.parametrize("name", ["gqa8_d128_unaligned", "peaky_logits", "ragged_mixed"])
+def test_prefill_with_more_splits_than_one_combine_round(name):
+    """19 key-range splits per query tile: the combine merges them in three
+    rounds of loads (8 + 8 + 3), rescaling when a later round raises the
+    row maximum (large logits make that likely)."""
+    h = _harness()
+    wl, o_ref, lse_ref, _, _ = cached_oracle(name)
+    print(f"case {name} splits=19", flush=True)
+    out, lse = h.DeviceBatch(wl).run(kv_splits=19)
+    torch.cuda.synchronize()
+    h.assert_parity(h.error_stats(h.host_bits(out), o_ref), f"{name}/splits=19")
+    assert np.abs(lse.cpu().numpy() - lse_ref).max() <= h.LSE_ABS
+
+
 @pytest.mark.parametrize("name", ["tiny", "ragged_mixed", "mha_d64_ps8", "gqa2_hkv2_ps64",
                                   "gqa16_ps256_d64", "cold_small"])
 def test_append_is_bit_exact_over_the_whole_pool(name):

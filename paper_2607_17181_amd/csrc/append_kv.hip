@@ -9,11 +9,15 @@
 //
 // Work unit: one workgroup per (logical page touched by the suffix,
 // sequence, KV head).  K rows move as 16-byte chunks (page rows are
-// contiguous in both layouts).  V pages are stored tokens-innermost, so each
-// thread assembles 8 consecutive slots of one feature row and writes them
-// with one 16-byte store when the whole group lies inside the suffix.  The
-// new rows are read once, so their loads are non-temporal; the pool stores
-// stay cached for the prefill that follows.
+// contiguous in both layouts).  V pages are stored tokens-innermost, so V
+// is transposed through LDS: the page's new V rows arrive with 16-byte loads
+// (token-major, each row padded by 16 bytes so that the column reads below
+// spread over the banks), and each thread then assembles 8 consecutive slots
+// of one feature row from LDS and writes them with one 16-byte store, a
+// wave's stores covering whole feature rows.  Groups of 8 slots that the
+// suffix only partly covers are written slot by slot.  The new rows are read
+// once, so their loads are non-temporal; the pool stores stay cached for the
+// prefill that follows.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -58,16 +62,25 @@ __global__ __launch_bounds__(256) void append_kv_kernel(PlanData p, const uint16
         *dst = __builtin_nontemporal_load(src);
     }
 
-    // V: page block [D][ps]; groups of 8 slots of one feature row.
+    // V: new rows -> LDS tile [ps][D] (row stride 2D + 16 bytes) -> page
+    // block [D][ps] in groups of 8 slots of one feature row.
+    extern __shared__ __attribute__((aligned(16))) char vt[];
+    constexpr int kRow = 2 * D + 16;
     const int slot_lo = pos_lo - lp * ps, slot_hi = pos_hi - lp * ps;
+    const int64_t row0 = s.tok_off + (lp * ps - s.prefix_len);  // row of slot 0 (may be < tok_off)
+    for (int c = threadIdx.x; c < ntok * CH; c += 256) {
+        const int sl = slot_lo + c / CH, col = c % CH;
+        const u32x4* src = reinterpret_cast<const u32x4*>(v_new + ((row0 + sl) * hkv + g) * D) + col;
+        *reinterpret_cast<u32x4*>(vt + sl * kRow + col * 16) = __builtin_nontemporal_load(src);
+    }
+    __syncthreads();
     const int grp_lo = slot_lo >> 3, grp_hi = (slot_hi + 7) >> 3;
     const int ngrp = grp_hi - grp_lo;
     uint16_t* vpage = v_pool + (page * hkv + g) * (int64_t)D * ps;
-    const int64_t row0 = s.tok_off + (lp * ps - s.prefix_len);  // row of slot 0 (may be < tok_off)
     for (int c = threadIdx.x; c < ngrp * D; c += 256) {
         const int d = c / ngrp;
-        const int grp = grp_lo + c % ngrp;
-        const int s0 = grp * 8;
+        const int s0 = (grp_lo + c % ngrp) * 8;
+        const char* col = vt + d * 2;
         uint16_t* dst = vpage + (int64_t)d * ps + s0;
         if (s0 >= slot_lo && s0 + 8 <= slot_hi) {
             union {
@@ -76,13 +89,13 @@ __global__ __launch_bounds__(256) void append_kv_kernel(PlanData p, const uint16
             } u;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                u.h[e] = __builtin_nontemporal_load(v_new + ((row0 + s0 + e) * hkv + g) * D + d);
+                u.h[e] = *reinterpret_cast<const uint16_t*>(col + (s0 + e) * kRow);
             *reinterpret_cast<u32x4*>(dst) = u.v;
         } else {
             for (int e = 0; e < 8; ++e) {
                 const int sl = s0 + e;
                 if (sl >= slot_lo && sl < slot_hi)
-                    dst[e] = v_new[((row0 + sl) * hkv + g) * D + d];
+                    dst[e] = *reinterpret_cast<const uint16_t*>(col + sl * kRow);
             }
         }
     }
@@ -111,11 +124,13 @@ extern "C" int talaria_sp_attn_append_kv(const talaria_sp_plan* plan, const void
     auto vn = static_cast<const uint16_t*>(v_new);
     auto kp = static_cast<uint16_t*>(k_pool);
     auto vp = static_cast<uint16_t*>(v_pool);
+    // LDS: one page of new V rows, padded.
+    const size_t lds = (size_t)p->page_size * (2 * p->head_dim + 16);
     if (p->head_dim == 128)
-        hipLaunchKernelGGL(append_kv_kernel<128>, grid, dim3(256), 0, st, *p, kn, vn, kp, vp,
+        hipLaunchKernelGGL(append_kv_kernel<128>, grid, dim3(256), lds, st, *p, kn, vn, kp, vp,
                            block_tables);
     else
-        hipLaunchKernelGGL(append_kv_kernel<64>, grid, dim3(256), 0, st, *p, kn, vn, kp, vp,
+        hipLaunchKernelGGL(append_kv_kernel<64>, grid, dim3(256), lds, st, *p, kn, vn, kp, vp,
                            block_tables);
     return launch_status("append_kv");
 }

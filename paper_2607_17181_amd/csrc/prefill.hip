@@ -123,6 +123,19 @@ __device__ __forceinline__ float xhalf_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Workgroup barrier without a memory fence.  A fenced barrier also waits for
+// every direct-to-LDS load still in flight (the loads issued for tiles
+// three and four ahead), which would expose their whole latency at every
+// tile.  Ordering is explicit instead: each wave waits for its own loads of
+// the tile that will be read (vmcnt) and for its LDS writes (lgkmcnt) before
+// the barrier; the empty asm statements keep the compiler from moving memory
+// accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ void wait_vmem_all() {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
@@ -483,7 +496,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     // P(t-1) is accumulated.
     auto sync_point = [&](int t) {
         wait_vmem_n<2 * G::LOADS>();
-        __syncthreads();
+        lds_barrier();
         // V(t+1) landed before this barrier: clear its keys past the end.
         if (t + 1 >= tb + 2 && t + 1 < te)
             zero_v_tail<D, SPAN, QB>(vbuf(t + 1), (t + 1) * kKeysPerTile, c.kv_len);

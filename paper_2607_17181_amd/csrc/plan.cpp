@@ -176,19 +176,41 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     double share = total_cost / concurrent;
     if (base_items >= concurrent)
         share *= 0.5;
-    const double target = std::max<double>(decode_batch ? kMinTilesPerDecodeSplit
-                                                        : kMinTilesPerSplit, share);
+    double target = std::max<double>(decode_batch ? kMinTilesPerDecodeSplit : kMinTilesPerSplit,
+                                     share);
+    auto splits_of = [&](int32_t b, double tgt) {
+        if (tiles[b] <= 0)
+            return 1;
+        const int32_t n = kv_splits > 0 ? kv_splits : (int32_t)ceil(tiles[b] / tgt * 0.999);
+        return std::max(1, std::min({n, tiles[b], kMaxSplits}));
+    };
+    // One round of items: every sequence rounds its split count up, which can
+    // push the total past the resident slots and leave a second round of
+    // items running alone at the end.  Raise the target (the fewest splits
+    // that fit) until the items fit; at `target` >= the longest key range
+    // every sequence has one split per query tile, i.e. base_items < slots.
+    if (kv_splits == 0 && base_items < concurrent) {
+        auto count = [&](double tgt) {
+            int64_t n = 0;
+            for (int32_t b = 0; b < num_seqs; ++b)
+                n += (int64_t)qtiles[b] * hkv * splits_of(b, tgt);
+            return n;
+        };
+        if (count(target) > concurrent) {
+            double lo = target, hi = 2.0 * target;
+            while (count(hi) > concurrent)
+                hi *= 2.0;
+            for (int i = 0; i < 40 && hi - lo > 1e-3; ++i) {
+                const double mid = 0.5 * (lo + hi);
+                (count(mid) > concurrent ? lo : hi) = mid;
+            }
+            target = hi;
+        }
+    }
 
     int64_t items = 0, part_items = 0;
     for (int32_t b = 0; b < num_seqs; ++b) {
-        int32_t nsp = 1;
-        if (tiles[b] > 0) {
-            if (kv_splits > 0)
-                nsp = kv_splits;
-            else
-                nsp = (int32_t)ceil(tiles[b] / target * 0.999);
-            nsp = std::max(1, std::min({nsp, tiles[b], kMaxSplits}));
-        }
+        const int32_t nsp = splits_of(b, target);
         p.seq[b].item_off = (int32_t)items;
         p.seq[b].part_off = (int32_t)part_items;
         const int64_t n = (int64_t)qtiles[b] * hkv * nsp;

@@ -96,6 +96,27 @@ def test_single_continuation_fills_the_gpu_in_one_round():
     assert sp.workspace_bytes == ((part + 255) // 256) * 256 + 256 * 256 * 4
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_items_fit_one_round_of_resident_slots(seed):
+    """A batch that cannot fill the GPU on its own is split into at most one
+    round of items: 256 slots for prefill (one workgroup per CU), 512 for a
+    decode batch (two per CU).  Per-sequence rounding must not spill over."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 65))
+    pre = np.minimum(rng.lognormal(np.log(25_000), 0.87, n), 131_072).astype(int).tolist()
+    decode = seed % 2 == 0
+    suf = [1] * n if decode else rng.integers(1, 33, size=n).tolist()
+    geom = _geom(pages=1 << 30)
+    sp = tsa.plan(geom, pre, suf, (max(pre) + max(suf) + 15) // 16)
+    items = check_coverage(sp, geom)
+    decode = max(suf) <= 1  # the planner's own test for a decode batch
+    assert items.shape[0] <= (512 if decode else 256)
+    # and not needlessly coarse: the longest item is within a few tiles of
+    # the mean (every split is at least one 64-key tile)
+    keys = items[:, 5] - items[:, 4]
+    assert keys.max() <= 1.25 * keys.mean() + 4 * 64
+
+
 def test_unsplit_batch_needs_no_workspace():
     sp = tsa.plan(_geom(), [0, 0, 0, 0], [25_000] * 4, 1600)
     assert sp.workspace_bytes == 0

@@ -597,17 +597,23 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     }
 }
 
-// Merge the split partials of one query tile.  Grid: (work item, row chunk of
-// 8 rows); only split 0 of a split tile does work.  Base-2 LSE merge in
-// split order.
+// Merge the split partials of one query tile, 8 rows per workgroup.  Only
+// split query tiles are launched (blocks past a sequence's own tile count,
+// or of sequences without splits, exit at once): a grid over every work
+// item spent most of its time dispatching blocks with nothing to do.
+// Base-2 LSE merge in split order.
 template <int D>
 __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* __restrict__ part_o,
                                                       const float* __restrict__ part_lse,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse) {
-    const WorkItem w = decode_item(p, blockIdx.x);
-    if (w.part_index < 0 || w.split != 0)
+    // Grid: (split query tile of the sequence, 8-row block, sequence); the
+    // tile's split 0 item is item_off + tile * splits.
+    const int32_t b = blockIdx.z;
+    const int32_t nsp = num_splits_of(p, b);
+    if (nsp <= 1 || (int32_t)blockIdx.x >= num_q_tiles(p, b) * p.num_kv_heads)
         return;
+    const WorkItem w = decode_item(p, p.seq[b].item_off + (int32_t)blockIdx.x * nsp);
     constexpr int TPR = D / 4;      // threads per row (4 features each)
     constexpr int RPB = 256 / TPR;  // rows per block
     const int r = blockIdx.y * RPB + threadIdx.x / TPR;
@@ -713,24 +719,27 @@ int launch_combine(const PlanData& p, const float* part_o, const float* part_lse
                    float* lse, hipStream_t st) {
     if (p.num_part_items == 0)
         return TALARIA_SP_OK;
-    // Rows of the tallest split query tile: the grid covers no more (a
-    // decode batch's split tiles hold `group` rows, not kRowsPerTile).
-    int32_t rows = 0;
+    // The grid covers only split query tiles: per sequence, as many tiles as
+    // the longest split sequence has, and the rows of the tallest split tile
+    // (a decode batch's split tiles hold `group` rows, not kRowsPerTile).
+    int32_t rows = 0, tiles = 0;
     for (int32_t b = 0; b < p.num_seqs; ++b)
         if (num_splits_of(p, b) > 1) {
             const int32_t t = p.seq[b].suffix_len < p.tile_tokens ? p.seq[b].suffix_len
                                                                   : p.tile_tokens;
             rows = rows > t * p.group ? rows : t * p.group;
+            const int32_t n = num_q_tiles(p, b) * p.num_kv_heads;
+            tiles = tiles > n ? tiles : n;
         }
     if (rows == 0)
         return TALARIA_SP_OK;
     if (p.head_dim == 128) {
         constexpr int RPB = 256 / (128 / 4);
-        hipLaunchKernelGGL(combine_kernel<128>, dim3(p.num_items, ceil_div(rows, RPB)), dim3(256),
+        hipLaunchKernelGGL(combine_kernel<128>, dim3(tiles, ceil_div(rows, RPB), p.num_seqs), dim3(256),
                            0, st, p, part_o, part_lse, out, lse);
     } else {
         constexpr int RPB = 256 / (64 / 4);
-        hipLaunchKernelGGL(combine_kernel<64>, dim3(p.num_items, ceil_div(rows, RPB)), dim3(256), 0,
+        hipLaunchKernelGGL(combine_kernel<64>, dim3(tiles, ceil_div(rows, RPB), p.num_seqs), dim3(256), 0,
                            st, p, part_o, part_lse, out, lse);
     }
     return launch_status("combine");

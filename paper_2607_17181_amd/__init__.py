@@ -1,7 +1,8 @@
 """Python binding of libtalaria_sp_attn (session-prefill attention on MI355X).
 
 Argument marshalling only: every step of the path (append, page gather,
-prefill, combine) runs in the HIP library.  There is no CPU fallback; if the
+prefill, combine, decode, page transfer, staging) runs in the HIP library,
+and batch selection in its host code.  There is no CPU fallback; if the
 library has not been built, every call raises.
 
 The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
@@ -9,8 +10,13 @@ The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
     sp = plan(geom, prefix_lens, suffix_lens, max_pages_per_seq)
     append_kv(sp, k_new, v_new, k_pool, v_pool, block_tables)
     prefill(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)
+    decode(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)   # S_b <= 1
+    gather_kv(sp, k_pool, v_pool, block_tables, k_out, v_out)
     hkvr_restore(cache, slab, page_ids, k_cache, v_cache)       # host -> device pages
     hkvr_checkpoint(cache, k_cache, v_cache, page_ids, slab)    # device pages -> host
+    stage_mark_dirty(chunks, used_pages, num_pages, page_bytes, dirty)
+    stage_gather(chunks, staged, dirty, staging, host_weights, weights)
+    sp_select(candidates, cost_model, budget)                    # host only
 
 Device arrays are ``torch`` tensors (bf16 data may also be passed as int16
 or uint16 bit patterns); torch provides device memory and the current

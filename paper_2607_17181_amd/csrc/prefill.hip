@@ -365,6 +365,10 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_o,
     float* __restrict__ part_lse) {
     using G = Geo<D, SPAN, QB>;
+    // The two-group schedule below (and its load distances) assumes 8 waves,
+    // two per SIMD, i.e. one 32-row block per wave.  The helpers take QB row
+    // blocks per wave so that a 64-row-per-wave layout can reuse them.
+    static_assert(QB == 1 && G::NW == 8, "the ping-pong schedule needs 8 waves of 32 rows");
     __shared__ __attribute__((aligned(1024))) char smem[(kKStages + kVStages) * G::TILE_BYTES];
 
     const WorkItem w = decode_item(p, blockIdx.x);

@@ -601,347 +601,6 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     }
 }
 
-// Four-phase schedule (32-key half-steps).  The K/V staging is the same as
-// above (64-key tiles through direct-to-LDS loads and per-wave page
-// loaders), but every half-step j runs four phases, each between two
-// workgroup barriers, and the two wave groups run one phase apart so that
-// one group computes while the other moves operands:
-//   P0 compute  S(j+1) = K(j+1) Q^T (8 MFMAs, K fragments already in
-//               registers), interleaved with the exponent part of the
-//               softmax of S(j) (P(j) to bf16 and the row sums);
-//   P1 memory   issue the tile loads two tiles ahead (every other
-//               half-step); V(j) fragments LDS -> registers, V entries past
-//               the end zeroed there; causal mask of S(j+1);
-//   P2 compute  O += V(j)^T P(j) (8 MFMAs), interleaved with the row maximum
-//               of S(j+1); then, if some row's maximum grew past the
-//               threshold, O and l are rescaled (O after P(j) went in);
-//   P3 memory   K(j+2) fragments LDS -> registers.
-// Group A (waves 0-3) passes a barrier after each phase, group B (waves
-// 4-7) before each, so B is one phase behind A.  MFMA operands come from
-// registers in the compute phases, so their MFMAs never wait on LDS.
-template <int D, int SPAN>
-__global__ __launch_bounds__(512, 1) void prefill4_kernel(
-    PlanData p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
-    const uint16_t* __restrict__ v_pool, const int32_t* __restrict__ bt, float sm_scale,
-    uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_o,
-    float* __restrict__ part_lse) {
-    using G = Geo<D, SPAN, 1>;
-    static_assert(G::NW == 8, "two groups of four waves");
-    constexpr int KS = D / 16, DB = D / 32;
-    constexpr int kAhead = 2;            // tiles in flight ahead of the one being read
-    constexpr int kRing = kAhead + 2;    // ring slots per operand (64-key tiles)
-    constexpr int kTileLoads = 2 * G::LOADS;  // direct loads per wave per tile (K + V)
-    __shared__ __attribute__((aligned(1024))) char smem[2 * kRing * G::TILE_BYTES];
-
-    const WorkItem w = decode_item(p, blockIdx.x);
-    const SeqDesc s = p.seq[w.seq];
-    const int Gq = p.group;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int lq = lane & 31;
-    const int lh = lane >> 5;
-    const bool group_b = wave >= G::NW / 2;
-
-    Ctx c;
-    c.page_bytes = (int64_t)p.num_kv_heads * p.page_size * D * 2;
-    c.kpool_g = reinterpret_cast<const char*>(k_pool) + (int64_t)w.kv_head * p.page_size * D * 2;
-    c.vpool_g = reinterpret_cast<const char*>(v_pool) + (int64_t)w.kv_head * p.page_size * D * 2;
-    c.bt_row = bt + (int64_t)w.seq * p.bt_stride;
-    c.kv_len = s.prefix_len + s.suffix_len;
-    c.page_shift = p.page_shift;
-    c.ps = p.page_size;
-    Loader<D, SPAN, 1> ld;
-    ld.init(wave, lane, c.ps);
-
-    // Query rows of this lane.
-    const int rows_used = p.tile_tokens * Gq;
-    const int r = wave * 32 + lq;
-    const int tq = r / Gq;
-    const bool valid = r < rows_used && tq < w.num_tokens;
-    const int qhead = w.kv_head * Gq + r % Gq;
-    const int qpos = s.prefix_len + w.first_token + (valid ? tq : w.num_tokens - 1);
-    bf16x8 qf[KS];
-    {
-        const uint16_t* src = q + ((int64_t)(s.tok_off + w.first_token + tq) * p.num_q_heads +
-                                   qhead) * D + lh * 8;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const u32x4 x = valid ? *reinterpret_cast<const u32x4*>(src + ks * 16)
-                                  : u32x4{0, 0, 0, 0};
-            qf[ks] = __builtin_bit_cast(bf16x8, x);
-        }
-    }
-    wait_vmem_all();  // Q is in; from here on only tile loads count in vmcnt
-
-    const int tb = w.tile_begin, te = w.tile_end;
-    auto kslot = [&](int t) -> char* { return smem + (t % kRing) * G::TILE_BYTES; };
-    auto vslot = [&](int t) -> char* { return smem + (kRing + t % kRing) * G::TILE_BYTES; };
-    // Unconditional: a tile past the end reads the sequence's last page into
-    // a slot nobody reads, and keeps every wave's vmcnt arithmetic uniform.
-    auto issue_tile = [&](int t) {
-        const int32_t pg = c.bt_row[ld.page_index(t * kKeysPerTile, c)];
-        ld.issue_k(kslot(t), t * kKeysPerTile, pg, c);
-        ld.issue_v(vslot(t), t * kKeysPerTile, pg, c);
-    };
-    // K rows of half-step j (32 keys) as A fragments, in the row order that
-    // puts S^T in the PV B-operand layout.
-    auto read_k = [&](int j, bf16x8 (&kf)[KS]) {
-        const char* kb = kslot(j >> 1);
-        const int row = (j & 1) * 32 + pi_row(lq);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            kf[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                kb + row * (2 * D) + (((2 * ks + lh) ^ kswz<D>(row)) << 4)));
-    };
-    // V^T fragments of half-step j; keys at or past the end are zeroed (the
-    // slots may hold anything, NaN included, and 0 * NaN is not 0).
-    auto read_v = [&](int j, bf16x8 (&vf)[2][DB]) {
-        const char* vt = vslot(j >> 1);
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-            const int key = (j & 1) * 32 + 16 * ks2 + 8 * lh;
-            const int pj = key / SPAN, lc = (key % SPAN) >> 3;
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d = db * 32 + lq;
-                vf[ks2][db] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                    vt + pj * G::V_BLOCK + d * (SPAN * 2) + ((lc ^ vswz<SPAN>(d)) << 4)));
-            }
-        }
-        if (j * 32 + 32 > c.kv_len) {
-#pragma unroll
-            for (int ks2 = 0; ks2 < 2; ++ks2) {
-                const int k0 = j * 32 + 16 * ks2 + 8 * lh;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    u32x4 x = __builtin_bit_cast(u32x4, vf[ks2][db]);
-#pragma unroll
-                    for (int e = 0; e < 8; e += 2)
-                        x[e / 2] &= (k0 + e < c.kv_len ? 0x0000FFFFu : 0u) |
-                                    (k0 + e + 1 < c.kv_len ? 0xFFFF0000u : 0u);
-                    vf[ks2][db] = __builtin_bit_cast(bf16x8, x);
-                }
-            }
-        }
-    };
-    auto qk = [&](const bf16x8 (&kf)[KS], f32x16& sv) {
-        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[0], f32x16{}, 0, 0, 0);
-#pragma unroll
-        for (int ks = 1; ks < KS; ++ks)
-            sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks], qf[ks], sv, 0, 0, 0);
-    };
-    // Keys past this row's position (the causal diagonal, and every key at
-    // or past the end) get -inf; only half-steps that reach past the first
-    // row of the query tile need it.
-    const int tile_first_pos = s.prefix_len + w.first_token;
-    auto mask_s = [&](int j, f32x16& sv) {
-        if (j * 32 + 31 > tile_first_pos) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                if (j * 32 + 16 * (e >> 3) + 8 * lh + (e & 7) > qpos)
-                    sv[e] = -INFINITY;
-        }
-    };
-    const float scale = sm_scale * kLog2e;
-    f32x16 o[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-        o[db] = f32x16{};
-    float m_run = -INFINITY, l_run = 0.f;
-    // Row maximum of S(j): raises m_run (and scales l_run) when some row's
-    // maximum grew past the threshold; returns the factor O needs, or 1.
-    auto row_max = [&](const f32x16& sv) -> float {
-        float m = max3f(sv[0], sv[1], sv[2]);
-#pragma unroll
-        for (int e = 3; e < 15; e += 2)
-            m = max3f(m, sv[e], sv[e + 1]);
-        m = __builtin_elementwise_maximum(m, sv[15]);
-        const float mt = xhalf_max(m) * scale;
-        float alpha = 1.f;
-        if (__any(mt > m_run + kRescaleThreshold)) {
-            const float mn = __builtin_fmaxf(m_run, mt);
-            alpha = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run - mn);
-            m_run = mn;
-            l_run *= alpha;
-        }
-        return alpha;
-    };
-    auto exp_part = [&](const f32x16& sv, bf16x8 (&pf)[2]) {
-        const float mb = (m_run == -INFINITY) ? 0.f : m_run;
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-            bf16x8 v;
-#pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[ks2 * 8 + e], scale, -mb));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[ks2 * 8 + e + 1], scale, -mb));
-                l_run += p0;
-                l_run += p1;
-                v[e] = (__bf16)p0;
-                v[e + 1] = (__bf16)p1;
-            }
-            pf[ks2] = v;
-        }
-    };
-    auto pv = [&](const bf16x8 (&vf)[2][DB], const bf16x8 (&pf)[2]) {
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2)
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[ks2][db], pf[ks2], o[db], 0,
-                                                                0, 0);
-    };
-
-    // Prologue: tiles tb and tb+1 in flight; S(2 tb) and its row maximum;
-    // K fragments of the half-step after it.
-    const int j0 = 2 * tb, jend = 2 * te;
-    bf16x8 kf[KS];
-    f32x16 s_a, s_b;
-    if (tb < te) {
-#pragma unroll
-        for (int t = 0; t < kAhead; ++t)
-            issue_tile(tb + t);
-        wait_vmem_n<(kAhead - 1) * kTileLoads>();
-        lds_barrier();
-        read_k(j0, kf);
-        qk(kf, s_a);
-        mask_s(j0, s_a);
-        row_max(s_a);
-        read_k(j0 + 1, kf);
-    }
-    // The four phases of half-step j, S(j) in `sc`, S(j+1) produced into `sn`.
-    bf16x8 pf[2];
-    bf16x8 vf[2][DB];
-    // Empty asm operands pin a value to a point in the phase order: the
-    // compiler otherwise moves pure arithmetic across the phase barriers
-    // (toward its uses), which would merge the phases.
-    auto pin_inputs0 = [&](f32x16& sc) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            asm volatile("" : "+v"(kf[ks]));
-        asm volatile("" : "+v"(sc));
-    };
-    auto phase0 = [&](f32x16& sc, f32x16& sn) {
-        __builtin_amdgcn_sched_barrier(0);
-        pin_inputs0(sc);
-        qk(kf, sn);
-        exp_part(sc, pf);
-#pragma unroll
-        for (int i = 0; i < KS; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);  // transcendental
-            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
-        }
-        asm volatile("" : "+v"(pf[0]), "+v"(pf[1]), "+v"(l_run));
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    auto phase1 = [&](int j, f32x16& sn) {
-        __builtin_amdgcn_sched_barrier(0);
-        if ((j & 1) == 0)
-            issue_tile((j >> 1) + kAhead);
-        read_v(j, vf);
-        mask_s(j + 1, sn);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    auto phase2 = [&](f32x16& sn) {
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2)
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-                asm volatile("" : "+v"(vf[ks2][db]));
-        pv(vf, pf);
-        const float alpha = row_max(sn);
-        if (alpha != 1.f) {
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-                o[db] *= alpha;
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    auto phase3 = [&](int j) {
-        __builtin_amdgcn_sched_barrier(0);
-        read_k(j + 2, kf);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    // The tile read first in P3 of an even half-step (two tiles back) must
-    // have landed in every wave before the barrier that opens that P3 for
-    // group A, which is the barrier that opens P2 for group B.
-    constexpr int kWait = (kAhead - 1) * kTileLoads;
-    if (!group_b) {
-        auto step = [&](int j, f32x16& sc, f32x16& sn) {
-            phase0(sc, sn);
-            lds_barrier();
-            phase1(j, sn);
-            lds_barrier();
-            phase2(sn);
-            if ((j & 1) == 0)
-                wait_vmem_n<kWait>();
-            lds_barrier();
-            phase3(j);
-            lds_barrier();
-        };
-        for (int j = j0; j < jend; j += 2) {
-            step(j, s_a, s_b);
-            step(j + 1, s_b, s_a);
-        }
-    } else {
-        auto step = [&](int j, f32x16& sc, f32x16& sn) {
-            lds_barrier();
-            phase0(sc, sn);
-            lds_barrier();
-            phase1(j, sn);
-            if ((j & 1) == 0)
-                wait_vmem_n<kWait>();
-            lds_barrier();
-            phase2(sn);
-            lds_barrier();
-            phase3(j);
-        };
-        for (int j = j0; j < jend; j += 2) {
-            step(j, s_a, s_b);
-            step(j + 1, s_b, s_a);
-        }
-    }
-
-    // Epilogue: full row sums, normalise, write.
-    const float l = xhalf_sum(l_run);
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    const float lse2 = l > 0.f ? m_run + __log2f(l) : -INFINITY;
-    if (!valid)
-        return;
-    if (w.part_index < 0) {
-        const int64_t row = (int64_t)(s.tok_off + w.first_token + tq) * p.num_q_heads + qhead;
-        uint16_t* dst = out + row * D;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int j4 = 0; j4 < 4; ++j4) {
-                bf16x4 v;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    v[e] = (__bf16)(o[db][j4 * 4 + e] * inv);
-                *reinterpret_cast<bf16x4*>(dst + db * 32 + j4 * 8 + lh * 4) = v;
-            }
-        if (lse && lh == 0)
-            lse[row] = lse2 * kLn2;
-    } else {
-        float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int j4 = 0; j4 < 4; ++j4) {
-                f32x4 v;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    v[e] = o[db][j4 * 4 + e] * inv;
-                *reinterpret_cast<f32x4*>(dst + db * 32 + j4 * 8 + lh * 4) = v;
-            }
-        if (lh == 0)
-            part_lse[(int64_t)w.part_index * kRowsPerTile + r] = lse2;
-    }
-}
-
 // Merge the split partials of one query tile, 8 rows per workgroup.  Only
 // split query tiles are launched (blocks past a sequence's own tile count,
 // or of sequences without splits, exit at once): a grid over every work
@@ -1022,22 +681,14 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
 
 // Rows per wave: 32 (8 waves, two per SIMD).
 constexpr int kQB = 1;
-#ifndef TSP_PREFILL4
-#define TSP_PREFILL4 0
-#endif
 
 template <int D, int SPAN>
 void launch_prefill_kernel(const PlanData& p, const uint16_t* q, const uint16_t* kp,
                            const uint16_t* vp, const int32_t* bt, float sm_scale, uint16_t* out,
                            float* lse, float* part_o, float* part_lse, hipStream_t st) {
-#if TSP_PREFILL4
-    hipLaunchKernelGGL((prefill4_kernel<D, SPAN>), dim3(p.num_items), dim3(512), 0, st, p, q, kp,
-                       vp, bt, sm_scale, out, lse, part_o, part_lse);
-#else
     hipLaunchKernelGGL((prefill_kernel<D, SPAN, kQB>), dim3(p.num_items),
                        dim3(Geo<D, SPAN, kQB>::NT), 0, st, p, q, kp, vp, bt, sm_scale, out, lse,
                        part_o, part_lse);
-#endif
 }
 
 template <int D>

@@ -94,6 +94,8 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     if (ps < 8 || ps > 256 || (ps & (ps - 1)) != 0)
         return fail(TALARIA_SP_EUNSUPPORTED, "page_size %d not supported (power of two in "
                     "[8, 256])", ps);
+    if ((int64_t)hkv * ps * d * 2 > INT32_MAX)
+        return fail(TALARIA_SP_EUNSUPPORTED, "one page of all %d KV heads exceeds 2 GiB", hkv);
     if (hq / hkv > kRowsPerTile)
         return fail(TALARIA_SP_EUNSUPPORTED, "query group %d exceeds %d", hq / hkv, kRowsPerTile);
     if (num_seqs < 0)

@@ -58,11 +58,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
+typedef __attribute__((address_space(1))) const char gbl_char;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 constexpr int kKStages = 4;  // K tile ring depth
+// Buffer descriptor of a page: no range clamp that a page offset could reach,
+// 32-bit data format (the raw-buffer setting).
+constexpr int kRsrcRecords = 0x7fffffff;
+constexpr int kRsrcFlags = 0x00020000;
 constexpr int kVStages = 5;  // V tile ring depth
 
 struct NoMask {
@@ -147,10 +152,11 @@ __device__ __forceinline__ void wait_vmem_n() {
 }
 
 struct Ctx {
-    const char* kpool_g;      // K pool + head offset (bytes)
-    const char* vpool_g;      // V pool + head offset (bytes)
+    const gbl_char* kpool_g;  // K pool + head offset (bytes)
+    const gbl_char* vpool_g;  // V pool + head offset (bytes)
     const int32_t* bt_row;    // block-table row of the sequence
-    int64_t page_bytes;       // bytes per page (all heads)
+    uint32_t page_bytes;      // bytes per page (all heads); the planner bounds it below 2^31
+    uint32_t last_page;       // block-table index of the sequence's last page
     int kv_len;               // P_b + S_b
     int page_shift;
     int ps;
@@ -188,29 +194,69 @@ struct Loader {
     // Block-table index of this wave's page for the tile at k0, clamped to
     // the sequence's last page (a tile past the end then reads keys that are
     // masked (K) or zeroed afterwards (V), from a page the sequence owns).
-    __device__ __forceinline__ int page_index(int k0, const Ctx& c) const {
-        return min((k0 + 8 * wave) >> c.page_shift, (c.kv_len - 1) >> c.page_shift);
+    __device__ __forceinline__ uint32_t page_index(uint32_t k0, const Ctx& c) const {
+        return min((k0 + 8u * (uint32_t)wave) >> c.page_shift, c.last_page);
     }
 
-    __device__ __forceinline__ void issue_k(char* buf, int k0, int32_t page,
-                                            const Ctx& c) const {
-        const char* base = c.kpool_g + (int64_t)page * c.page_bytes +
-                           (int64_t)(k0 & (c.ps - 1)) * (D * 2);
+    // The loads use the buffer form of the direct-to-LDS load: a descriptor
+    // built (in scalar registers) for the wave's page, plus the per-lane
+    // 32-bit offset.  Unlike the global form, the compiler counts these loads
+    // on the vector-memory counter only, so LDS reads issued while they are
+    // in flight keep exact (not drain-all) waits.
+    __device__ __forceinline__ void issue(const gbl_char* pool, const uint32_t (&off)[G::LOADS],
+                                          uint32_t in_page, char* buf, uint32_t page,
+                                          const Ctx& c) const {
+        const gbl_char* base = pool + (uint64_t)page * c.page_bytes + in_page;
+        const __amdgpu_buffer_rsrc_t rsrc =
+            __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, kRsrcRecords, kRsrcFlags);
 #pragma unroll
         for (int i = 0; i < G::LOADS; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void*)(base + koff[i]),
-                                             (lds_void*)(buf + (wave * G::LOADS + i) * 1024), 16,
-                                             0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsrc, (lds_void*)(buf + (wave * G::LOADS + i) * 1024), 16, off[i], 0, 0, 0);
     }
-    __device__ __forceinline__ void issue_v(char* buf, int k0, int32_t page,
+    __device__ __forceinline__ void issue_k(char* buf, uint32_t k0, uint32_t page,
                                             const Ctx& c) const {
-        const char* base = c.vpool_g + (int64_t)page * c.page_bytes +
-                           (int64_t)(k0 & (c.ps - 1)) * 2;
+        issue(c.kpool_g, koff, (k0 & (uint32_t)(c.ps - 1)) * (D * 2), buf, page, c);
+    }
+    __device__ __forceinline__ void issue_v(char* buf, uint32_t k0, uint32_t page,
+                                            const Ctx& c) const {
+        issue(c.vpool_g, voff, (k0 & (uint32_t)(c.ps - 1)) * 2, buf, page, c);
+    }
+};
+
+// Per-lane LDS byte offsets of the MFMA operand reads, fixed for the whole
+// kernel.  K: one per 16-wide k-step (the second 32-key block is a constant
+// 32 rows further).  V: the key pairs of a 16-key step and the 32-feature
+// blocks are constant strides when a page block holds at most 16 keys;
+// wider blocks swizzle the key chunk by feature row, so each 16-key step
+// has its own offset.
+template <int D, int SPAN, int QB>
+struct OperandOffsets {
+    using G = Geo<D, SPAN, QB>;
+    static constexpr bool V_UNIFORM_STEP = SPAN <= 16;
+    static constexpr int VN = V_UNIFORM_STEP ? 1 : 4;
+    uint32_t k[D / 16];
+    uint32_t v[VN];
+
+    __device__ __forceinline__ void init(int lq, int lh) {
+        const int row = pi_row(lq);
 #pragma unroll
-        for (int i = 0; i < G::LOADS; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void*)(base + voff[i]),
-                                             (lds_void*)(buf + (wave * G::LOADS + i) * 1024), 16,
-                                             0, 0);
+        for (int ks = 0; ks < D / 16; ++ks)
+            k[ks] = (uint32_t)(row * (2 * D) + (((2 * ks + lh) ^ kswz<D>(row)) << 4));
+#pragma unroll
+        for (int j = 0; j < VN; ++j) {
+            // Block row d = 32 db + lq has the swizzle of lq (the swizzles
+            // only look at the low five bits of d).
+            const int key = 16 * j + 8 * lh;
+            const int pj = key / SPAN, lc = (key % SPAN) >> 3;
+            v[j] = (uint32_t)(pj * G::V_BLOCK + lq * (SPAN * 2) + ((lc ^ vswz<SPAN>(lq)) << 4));
+        }
+    }
+    // Offset of the V operand of 16-key step ks2 and feature block db.
+    __device__ __forceinline__ const char* vptr(const char* vt, int ks2, int db) const {
+        if (V_UNIFORM_STEP)
+            return vt + v[0] + ks2 * (16 / SPAN) * G::V_BLOCK + db * 32 * SPAN * 2;
+        return vt + v[ks2] + db * 32 * SPAN * 2;
     }
 };
 
@@ -235,7 +281,8 @@ __device__ __forceinline__ void zero_v_tail(char* vbuf, int k0, int kv_len) {
 // S^T = K Q^T for the wave's QB 32-row blocks.
 template <int D, int SPAN, int QB>
 __device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* kbuf,
-                                        const bf16x8 (&qf)[QB][D / 16], int lq, int lh) {
+                                        const bf16x8 (&qf)[QB][D / 16],
+                                        const OperandOffsets<D, SPAN, QB>& oo) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -243,12 +290,10 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* kbuf,
             s[qb][kb] = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
+        const char* kp = kbuf + oo.k[ks];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-            const int row = kb * 32 + pi_row(lq);
-            const int lc = 2 * ks + lh;
-            const u32x4 a = *reinterpret_cast<const u32x4*>(
-                kbuf + row * (2 * D) + ((lc ^ kswz<D>(row)) << 4));
+            const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kb * 32 * (2 * D));
             const bf16x8 af = __builtin_bit_cast(bf16x8, a);
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb)
@@ -261,17 +306,13 @@ __device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* kbuf,
 // O^T += V^T P^T for the wave's QB 32-row blocks.
 template <int D, int SPAN, int QB>
 __device__ __forceinline__ void pv_tile(f32x16 (&o)[QB][D / 32], const char* vt,
-                                        const bf16x8 (&pf)[QB][4], int lq, int lh) {
-    using G = Geo<D, SPAN, QB>;
+                                        const bf16x8 (&pf)[QB][4],
+                                        const OperandOffsets<D, SPAN, QB>& oo) {
 #pragma unroll
     for (int ks2 = 0; ks2 < 4; ++ks2) {
-        const int key = 16 * ks2 + 8 * lh;
-        const int pj = key / SPAN, lc = (key % SPAN) >> 3;
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-            const int d = db * 32 + lq;
-            const u32x4 a = *reinterpret_cast<const u32x4*>(
-                vt + pj * G::V_BLOCK + d * (SPAN * 2) + ((lc ^ vswz<SPAN>(d)) << 4));
+            const u32x4 a = *reinterpret_cast<const u32x4*>(oo.vptr(vt, ks2, db));
             const bf16x8 af = __builtin_bit_cast(bf16x8, a);
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb)
@@ -380,22 +421,34 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     const int lh = lane >> 5;
 
     Ctx c;
-    c.page_bytes = (int64_t)p.num_kv_heads * p.page_size * D * 2;
-    c.kpool_g = reinterpret_cast<const char*>(k_pool) + (int64_t)w.kv_head * p.page_size * D * 2;
-    c.vpool_g = reinterpret_cast<const char*>(v_pool) + (int64_t)w.kv_head * p.page_size * D * 2;
+    c.page_bytes = (uint32_t)(p.num_kv_heads * p.page_size * D * 2);
+    c.kpool_g = (const gbl_char*)(const char*)k_pool + (int64_t)w.kv_head * p.page_size * D * 2;
+    c.vpool_g = (const gbl_char*)(const char*)v_pool + (int64_t)w.kv_head * p.page_size * D * 2;
     c.bt_row = bt + (int64_t)w.seq * p.bt_stride;
     c.kv_len = s.prefix_len + s.suffix_len;
     c.page_shift = p.page_shift;
+    c.last_page = (uint32_t)(c.kv_len - 1) >> p.page_shift;
     c.ps = p.page_size;
 
     Loader<D, SPAN, QB> ld;
     ld.init(wave, lane, c.ps);
+    OperandOffsets<D, SPAN, QB> oo;
+    oo.init(lq, lh);
 
     const int tb = w.tile_begin, te = w.tile_end;
-    // Ring slots: K tile t in kbuf(t), V tile t in vbuf(t).
-    auto kbuf = [&](int t) -> char* { return smem + (t % kKStages) * G::TILE_BYTES; };
-    auto vbuf = [&](int t) -> char* {
-        return smem + (kKStages + t % kVStages) * G::TILE_BYTES;
+    // Ring slots: K tile t in kbuf(t), V tile t in vbuf(t).  Inside the main
+    // loop the slots in use are carried as byte offsets and stepped once per
+    // tile (no modulo per access).
+    constexpr uint32_t TB = G::TILE_BYTES;
+    constexpr uint32_t KRING = kKStages * TB;
+    static_assert((KRING & (KRING - 1)) == 0, "K ring size must be a power of two");
+    auto kslot = [&](int t) -> uint32_t { return (uint32_t)(t % kKStages) * TB; };
+    auto vslot = [&](int t) -> uint32_t { return KRING + (uint32_t)(t % kVStages) * TB; };
+    auto kbuf = [&](int t) -> char* { return smem + kslot(t); };
+    auto vbuf = [&](int t) -> char* { return smem + vslot(t); };
+    auto knext = [](uint32_t x) -> uint32_t { return (x + TB) & (KRING - 1); };
+    auto vnext = [](uint32_t x) -> uint32_t {
+        return x + TB == KRING + kVStages * TB ? KRING : x + TB;
     };
 
     // Load schedule.  In iteration t every wave issues its share of
@@ -417,8 +470,8 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         if (k < vd)
             ld.issue_v(vbuf(tb + k), (tb + k) * kKeysPerTile,
                        c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
-    int32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
-    int32_t pgv_next = c.bt_row[ld.page_index((tb + vd) * kKeysPerTile, c)];
+    uint32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
+    uint32_t pgv_next = c.bt_row[ld.page_index((tb + vd) * kKeysPerTile, c)];
 
     // Query rows of this lane: one per 32-row block.
     const int rows_used = p.tile_tokens * Gq;
@@ -465,10 +518,6 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     }
     wait_vmem_all();
     __syncthreads();
-#pragma unroll
-    for (int k = 0; k < 2; ++k)
-        if (tb + k < te)
-            zero_v_tail<D, SPAN, QB>(vbuf(tb + k), (tb + k) * kKeysPerTile, c.kv_len);
 
     f32x16 sc[QB][2];
     bf16x8 pf[QB][4];
@@ -478,7 +527,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         for (int k = 0; k < 4; ++k)
             pf[qb][k] = bf16x8{};
     if (tb < te)
-        qk_tile<D, SPAN, QB>(sc, kbuf(tb), qf, lq, lh);
+        qk_tile<D, SPAN, QB>(sc, kbuf(tb), qf, oo);
 
     // tmask = smallest t with t * 64 + 63 > tile_first_pos (first tile that
     // can hold keys past some row of the query tile).
@@ -497,22 +546,36 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     // the previous barrier (the 2 * LOADS issued since may stay in flight).
     // Invariant at the start of iteration t: sc = S(t), pf = P(t-1); a pending
     // rescale (resc, alpha) from softmax(t-1) is applied to O just before
-    // P(t-1) is accumulated.
-    auto sync_point = [&](int t) {
+    // P(t-1) is accumulated.  Slots: k_rd holds K(t+1), k_wr receives
+    // K(t+kd), v_rd holds V(t-1), v_wr receives V(t+vd).
+    uint32_t k_rd = kslot(tb + 1), k_wr = kslot(tb + kd);
+    uint32_t v_rd = vslot(tb - 1 + kVStages), v_wr = vslot(tb + vd);
+    auto sync_point = [&]() {
         wait_vmem_n<2 * G::LOADS>();
         lds_barrier();
-        // V(t+1) landed before this barrier: clear its keys past the end.
-        if (t + 1 >= tb + 2 && t + 1 < te)
-            zero_v_tail<D, SPAN, QB>(vbuf(t + 1), (t + 1) * kKeysPerTile, c.kv_len);
     };
     auto iteration = [&](int t, auto mask_tag) {
         constexpr bool MASK = decltype(mask_tag)::value;
+        // Pages of the next iteration's loads.  The scalar loads are issued
+        // here and waited for after the softmax (which has no LDS traffic):
+        // while a scalar load is outstanding every LDS wait must drain all
+        // LDS reads, which would serialise the MFMA phase's operand reads.
+        const uint32_t pk = c.bt_row[ld.page_index((uint32_t)(t + 1 + kd) * kKeysPerTile, c)];
+        const uint32_t pv = c.bt_row[ld.page_index((uint32_t)(t + 1 + vd) * kKeysPerTile, c)];
         bf16x8 pn[QB][4];
         float an[QB];
         const bool rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile,
                                                qpos, lh);
+        // The whole softmax step completes here, ahead of the MFMA phase (the
+        // compiler would otherwise sink its exp/convert tail past it).
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                asm volatile("" ::"v"(pn[qb][k]));
+        asm volatile("" ::"s"(pk), "s"(pv));
         if (group_b)
-            sync_point(t);
+            sync_point();
         __builtin_amdgcn_sched_barrier(0);
         if (resc) {
 #pragma unroll
@@ -523,12 +586,25 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         }
         // MFMA phase, unconditional: P(tb-1) = 0 over a zeroed V stage, and
         // S(te) comes from a stale slot and is never used.
-        pv_tile<D, SPAN, QB>(o, vbuf(t - 1 + kVStages), pf, lq, lh);
-        ld.issue_k(kbuf(t + kd), (t + kd) * kKeysPerTile, pgk_next, c);
-        ld.issue_v(vbuf(t + vd), (t + vd) * kKeysPerTile, pgv_next, c);
-        qk_tile<D, SPAN, QB>(sc, kbuf(t + 1), qf, lq, lh);
-        pgk_next = c.bt_row[ld.page_index((t + 1 + kd) * kKeysPerTile, c)];
-        pgv_next = c.bt_row[ld.page_index((t + 1 + vd) * kKeysPerTile, c)];
+        pv_tile<D, SPAN, QB>(o, smem + v_rd, pf, oo);
+        ld.issue_k(smem + k_wr, (uint32_t)(t + kd) * kKeysPerTile, pgk_next, c);
+        ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
+        qk_tile<D, SPAN, QB>(sc, smem + k_rd, qf, oo);
+        // Operand reads run four ahead of the MFMAs that use them, across the
+        // PV / QK boundary: 4 reads, then (MFMA, read) pairs, then 4 MFMAs.
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+        for (int i = 0; i < 2 * 16 * QB - 4; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        pgk_next = pk;
+        pgv_next = pv;
+        k_rd = knext(k_rd);
+        k_wr = knext(k_wr);
+        v_rd = vnext(v_rd);
+        v_wr = vnext(v_wr);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
@@ -538,7 +614,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         }
         resc = rn;
         if (!group_b)
-            sync_point(t);
+            sync_point();
     };
 
     const int split = tmask < tb ? tb : (tmask > te ? te : tmask);
@@ -548,6 +624,16 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         iteration(t, WithMask{});
 
     if (tb < te) {
+        // Of this item's tiles only the last one can reach past the sequence's
+        // end (every earlier tile ends below the item's visible key count,
+        // which is at most P_b + S_b), and it is read only here: clear its V
+        // entries past the end once, now that it has landed.
+        if (te * kKeysPerTile > c.kv_len) {
+            wait_vmem_all();
+            __syncthreads();
+            zero_v_tail<D, SPAN, QB>(vbuf(te - 1), (te - 1) * kKeysPerTile, c.kv_len);
+            __syncthreads();
+        }
         if (resc) {
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb)
@@ -555,7 +641,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
                 for (int db = 0; db < D / 32; ++db)
                     o[qb][db] *= alpha[qb];
         }
-        pv_tile<D, SPAN, QB>(o, vbuf(te - 1), pf, lq, lh);
+        pv_tile<D, SPAN, QB>(o, vbuf(te - 1), pf, oo);
     }
 
     // Epilogue: full row sums, normalise, write.

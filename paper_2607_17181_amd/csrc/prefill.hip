@@ -377,7 +377,9 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const float mb = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
-        float ls = l_run[qb];
+        // Four independent partial row sums (one per 16-key step), so the
+        // adds do not form one 32-long dependency chain.
+        float ls[4];
 #pragma unroll
         for (int ks2 = 0; ks2 < 4; ++ks2) {
             bf16x8 v;
@@ -387,14 +389,13 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB
                     fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e], scale, -mb));
                 const float p1 = __builtin_amdgcn_exp2f(
                     fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e + 1], scale, -mb));
-                ls += p0;
-                ls += p1;
+                ls[ks2] = e == 0 ? p0 + p1 : ls[ks2] + p0 + p1;
                 v[e] = (__bf16)p0;
                 v[e + 1] = (__bf16)p1;
             }
             pf[qb][ks2] = v;
         }
-        l_run[qb] = ls;
+        l_run[qb] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
     }
     return resc;
 }
@@ -554,7 +555,8 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         wait_vmem_n<2 * G::LOADS>();
         lds_barrier();
     };
-    auto iteration = [&](int t, auto mask_tag) {
+    auto iteration = [&](int t, auto mask_tag, const bf16x8 (&pf)[QB][4],
+                         bf16x8 (&pn)[QB][4]) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask_tag)::value;
         // Pages of the next iteration's loads.  The scalar loads are issued
         // here and waited for after the softmax (which has no LDS traffic):
@@ -562,21 +564,26 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         // LDS reads, which would serialise the MFMA phase's operand reads.
         const uint32_t pk = c.bt_row[ld.page_index((uint32_t)(t + 1 + kd) * kKeysPerTile, c)];
         const uint32_t pv = c.bt_row[ld.page_index((uint32_t)(t + 1 + vd) * kKeysPerTile, c)];
-        bf16x8 pn[QB][4];
         float an[QB];
         const bool rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile,
                                                qpos, lh);
         // The whole softmax step completes here, ahead of the MFMA phase (the
-        // compiler would otherwise sink its exp/convert tail past it).
+        // compiler would otherwise sink its exp/convert/sum tail past it).
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
+        for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
             for (int k = 0; k < 4; ++k)
                 asm volatile("" ::"v"(pn[qb][k]));
+            asm volatile("" ::"v"(l_run[qb]));
+        }
         asm volatile("" ::"s"(pk), "s"(pv));
         if (group_b)
             sync_point();
         __builtin_amdgcn_sched_barrier(0);
+        // The MFMA phase runs at raised wave priority: its SIMD partner is in
+        // its softmax, and without this the partner's VALU stream (an older
+        // wave for group B) wins issue slots and stretches the MFMA phase.
+        __builtin_amdgcn_s_setprio(1);
         if (resc) {
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb)
@@ -599,6 +606,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
         __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        __builtin_amdgcn_s_setprio(0);
         pgk_next = pk;
         pgv_next = pv;
         k_rd = knext(k_rd);
@@ -606,22 +614,34 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         v_rd = vnext(v_rd);
         v_wr = vnext(v_wr);
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                pf[qb][k] = pn[qb][k];
+        for (int qb = 0; qb < QB; ++qb)
             alpha[qb] = an[qb];
-        }
         resc = rn;
         if (!group_b)
             sync_point();
     };
 
+    // P alternates between two register sets, two iterations per loop trip,
+    // so that no copy is needed: at the start of a trip P(t-1) is in pf.
+    bf16x8 pn[QB][4];
+    auto run = [&](int t0, int t1, auto mask_tag) __attribute__((always_inline)) {
+        int t = t0;
+        for (; t + 1 < t1; t += 2) {
+            iteration(t, mask_tag, pf, pn);
+            iteration(t + 1, mask_tag, pn, pf);
+        }
+        if (t < t1) {
+            iteration(t, mask_tag, pf, pn);
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    pf[qb][k] = pn[qb][k];
+        }
+    };
     const int split = tmask < tb ? tb : (tmask > te ? te : tmask);
-    for (int t = tb; t < split; ++t)
-        iteration(t, NoMask{});
-    for (int t = split; t < te; ++t)
-        iteration(t, WithMask{});
+    run(tb, split, NoMask{});
+    run(split, te, WithMask{});
 
     if (tb < te) {
         // Of this item's tiles only the last one can reach past the sequence's

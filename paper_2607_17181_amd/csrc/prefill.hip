@@ -453,14 +453,13 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     };
 
     // Load schedule.  In iteration t every wave issues its share of
-    // K(t + kd) and V(t + vd) from inside its MFMA phase, kd = 3 / vd = 2 for
-    // group A and kd = 4 / vd = 3 for group B (group A's MFMA phase precedes
-    // barrier t, group B's follows it), so in both groups the loads issued
-    // between barriers b-1 and b are K(b+4)/V(b+3)'s.  The prologue loads the
-    // tiles the first iterations need.  Loads are unconditional: a tile past
-    // the end reads the sequence's last page into a ring slot nobody reads.
+    // K(t + kd) and V(t + vd), kd = 3 / vd = 2, at the start of the
+    // iteration, which in both groups falls between barriers t-1 and t.  The
+    // prologue loads the tiles the first iterations need.  Loads are
+    // unconditional: a tile past the end reads the sequence's last page into
+    // a ring slot nobody reads.
     const bool group_b = wave >= G::NW / 2;
-    const int kd = group_b ? 4 : 3, vd = group_b ? 3 : 2;
+    constexpr int kd = 3, vd = 2;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
         if (k < kd)
@@ -565,6 +564,10 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         const uint32_t pk = c.bt_row[ld.page_index((uint32_t)(t + 1 + kd) * kKeysPerTile, c)];
         const uint32_t pv = c.bt_row[ld.page_index((uint32_t)(t + 1 + vd) * kKeysPerTile, c)];
         float an[QB];
+        // This iteration's tile loads, issued before the softmax so that the
+        // MFMA phase holds only operand reads and MFMAs.
+        ld.issue_k(smem + k_wr, (uint32_t)(t + kd) * kKeysPerTile, pgk_next, c);
+        ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
         const bool rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile,
                                                qpos, lh);
         // The whole softmax step completes here, ahead of the MFMA phase (the
@@ -594,8 +597,6 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         // MFMA phase, unconditional: P(tb-1) = 0 over a zeroed V stage, and
         // S(te) comes from a stale slot and is never used.
         pv_tile<D, SPAN, QB>(o, smem + v_rd, pf, oo);
-        ld.issue_k(smem + k_wr, (uint32_t)(t + kd) * kKeysPerTile, pgk_next, c);
-        ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
         qk_tile<D, SPAN, QB>(sc, smem + k_rd, qf, oo);
         // Operand reads run four ahead of the MFMAs that use them, across the
         // PV / QK boundary: 4 reads, then (MFMA, read) pairs, then 4 MFMAs.

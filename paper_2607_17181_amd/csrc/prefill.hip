@@ -63,6 +63,7 @@ typedef __attribute__((address_space(1))) const char gbl_char;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
+constexpr float kMaxLazyP = 256.0f;        // 2^kRescaleThreshold
 constexpr int kKStages = 4;  // K tile ring depth
 // Buffer descriptor of a page: no range clamp that a page offset could reach,
 // 32-bit data format (the raw-buffer setting).
@@ -400,6 +401,50 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB
     return resc;
 }
 
+// Optimistic softmax step for a tile without masked keys: P(t) with the
+// running max as it stands, skipping the row maximum.  softmax_tile would
+// leave the max where it is exactly when no P value exceeds 2^8, and then
+// both compute the same P and row sums.  A lane's partial row sum bounds its
+// P values, so the step is accepted when no lane's sum exceeds 2^8 (and
+// every row already has a finite running max); otherwise the caller redoes
+// the tile with softmax_tile.  Returns whether the step was accepted.
+template <int QB>
+__device__ __forceinline__ bool softmax_fast(const f32x16 (&s)[QB][2], bf16x8 (&pf)[QB][4],
+                                             const float (&m_run)[QB], float (&l_run)[QB],
+                                             float scale) {
+    bool bad = false;
+    float lsum[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const float mb = m_run[qb];
+        bad = bad || (mb == -INFINITY);
+        float ls[4];
+#pragma unroll
+        for (int ks2 = 0; ks2 < 4; ++ks2) {
+            bf16x8 v;
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(
+                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e], scale, -mb));
+                const float p1 = __builtin_amdgcn_exp2f(
+                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e + 1], scale, -mb));
+                ls[ks2] = e == 0 ? p0 + p1 : ls[ks2] + p0 + p1;
+                v[e] = (__bf16)p0;
+                v[e + 1] = (__bf16)p1;
+            }
+            pf[qb][ks2] = v;
+        }
+        lsum[qb] = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+        bad = bad || !(lsum[qb] <= kMaxLazyP);
+    }
+    if (__any(bad))
+        return false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+        l_run[qb] += lsum[qb];
+    return true;
+}
+
 template <int D, int SPAN, int QB>
 __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     PlanData p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
@@ -568,8 +613,10 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         // MFMA phase holds only operand reads and MFMAs.
         ld.issue_k(smem + k_wr, (uint32_t)(t + kd) * kKeysPerTile, pgk_next, c);
         ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
-        const bool rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile,
-                                               qpos, lh);
+        bool rn = false;
+        if (MASK || !softmax_fast<QB>(sc, pn, m_run, l_run, scale))
+            rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile, qpos,
+                                        lh);
         // The whole softmax step completes here, ahead of the MFMA phase (the
         // compiler would otherwise sink its exp/convert/sum tail past it).
 #pragma unroll

@@ -9,13 +9,13 @@
 // LDS serves all of them -- against one contiguous range of 64-key tiles.
 // Each wave owns one 32-row MFMA block.
 //
-// Data movement.  K/V tiles move HBM -> LDS with global_load_lds_dwordx4
-// (no register staging) into two rings, K four tiles deep and V five: all
-// of a wave's loads of one tile stay inside one page, so its page id is one
-// wave-uniform block-table load and the per-lane part of each address is
-// loop-invariant.  Keys at or past P_b + S_b are never fetched from unowned
-// pages; V entries past the end are zeroed in LDS so stale slots (even NaN)
-// cannot reach the output.
+// Data movement.  K/V tiles move HBM -> LDS with the buffer form of the
+// direct-to-LDS load (no register staging) into two rings, K four tiles deep
+// and V five: all of a wave's loads of one tile stay inside one page, so its
+// page id is one wave-uniform block-table load and the per-lane part of each
+// address is loop-invariant.  Keys at or past P_b + S_b are never fetched
+// from unowned pages; V entries past the end are zeroed in LDS so stale
+// slots (even NaN) cannot reach the output.
 //   K tile in LDS: 64 keys x D, natural key order, 16-byte chunks XOR-swizzled
 //                  by row.
 //   V tile in LDS: per page, [D][span] (tokens innermost, as in the pool),
@@ -27,14 +27,18 @@
 // no transpose.
 //
 // Pipeline (per wave, one iteration per key tile t):
-//     P(t) = softmax step on S(t)  VALU: max, permlane32 swap, fma, exp2,
-//                                  cvt_pk_bf16, fp32 row sums
+//     P(t) = softmax step on S(t)  VALU: fma, exp2, cvt_pk_bf16, fp32 row
+//                                  sums (and, when needed, the row max with
+//                                  a permlane32 swap)
 //     O   += V(t-1)^T P(t-1)      D/8 x v_mfma_f32_32x32x16_bf16
 //     S(t+1) = K(t+1) Q^T          D/8 x MFMA
 // The two waves of a SIMD are one phase apart, so one wave's softmax runs
-// while the other's MFMAs do.  The
-// running maximum is lazy: O and l are rescaled only when some row's maximum
-// grows by more than 2^8, so exp2 arguments stay <= 8.
+// while the other's MFMAs do; the MFMA phase runs at raised wave priority.
+// The running maximum is lazy: O and l are rescaled only when some row's
+// maximum grows by more than 2^8, so exp2 arguments stay <= 8.  Unmasked
+// tiles first try the step with the running max as it stands and fall back
+// to the full step (with the row max) only when some P value could exceed
+// 2^8.
 //
 // Items whose query tile is split over several key ranges write normalised
 // fp32 partials and base-2 LSE to the workspace; the combine kernel merges
@@ -57,7 +61,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) const void gbl_void;
 typedef __attribute__((address_space(1))) const char gbl_char;
 
 constexpr float kLog2e = 1.4426950408889634f;

@@ -250,3 +250,52 @@ def test_full_size_config_sampled_rows(name):
     h.assert_parity(h.error_stats(gpu_rows, o_ref), name)
     lse_gpu = lse.cpu().numpy().reshape(-1)[rows]
     assert np.abs(lse_gpu - lse_ref).max() <= h.LSE_ABS
+
+
+def _logit_levels(name, levels, pre=1000, suf=200):
+    """Single-sequence workload whose logits are set by key position: every
+    query is the first unit vector, and key j has log2-unit logit
+    levels(j) (its first feature carries it, the rest are zero), so whole
+    key tiles can be placed above or below the running maximum."""
+    from workload import bf16_bits_from_f32
+    wl = _small(name, 8, 1, 128, 16, [pre], [suf])
+    d = wl.head_dim
+    unit = np.log2(np.e) / np.sqrt(d)  # log2-unit logit per unit of k[0] when q = e0
+    qf = np.zeros(wl.q.shape, dtype=np.float32)
+    qf[..., 0] = 1.0
+    wl.q = bf16_bits_from_f32(qf)
+
+    def keys(pos, hkv):
+        kf = np.zeros((pos.shape[0], hkv, d), dtype=np.float32)
+        kf[..., 0] = (levels(pos) / unit)[:, None]
+        return bf16_bits_from_f32(kf)
+
+    wl.prefix_k = keys(np.arange(pre), wl.num_kv_heads)
+    wl.k_new = keys(pre + np.arange(suf), wl.num_kv_heads)
+    return wl
+
+
+LOGIT_LEVELS = {
+    # Every tile after the first sits 3.5 (log2) above the running max: the
+    # optimistic step's lane sums exceed 2^8 and it is redone by the full
+    # step, which does not move the max (3.5 < 8).
+    "rejected_without_rescale": lambda: _logit_levels(
+        "k", lambda j: np.where(j < 64, 0.0, 3.5)),
+    # Each key tile sits 10 (log2) above the previous one: the running max
+    # moves, and O and the row sums are rescaled, at every tile.
+    "rescale_every_tile": lambda: _logit_levels(
+        "l", lambda j: 10.0 * (j // 64)),
+}
+
+
+@pytest.mark.parametrize("splits", [0, 1, 5])
+@pytest.mark.parametrize("name", list(LOGIT_LEVELS))
+def test_prefill_softmax_paths_match_oracle(name, splits):
+    h = _harness()
+    wl = LOGIT_LEVELS[name]()
+    o_ref, lse_ref, _, _ = oracle_outputs(wl)
+    print(f"case {name} splits={splits}", flush=True)
+    out, lse = h.DeviceBatch(wl).run(kv_splits=splits)
+    torch.cuda.synchronize()
+    h.assert_parity(h.error_stats(h.host_bits(out), o_ref), f"{name}/splits={splits}")
+    assert np.abs(lse.cpu().numpy() - lse_ref).max() <= h.LSE_ABS

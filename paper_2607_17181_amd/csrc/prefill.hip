@@ -67,6 +67,8 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 constexpr float kMaxLazyP = 256.0f;        // 2^kRescaleThreshold
+static_assert(kRescaleThreshold == 8.0f && kMaxLazyP == 256.0f,
+              "the optimistic softmax bound must equal 2^kRescaleThreshold");
 constexpr int kKStages = 4;  // K tile ring depth
 // Buffer descriptor of a page: no range clamp that a page offset could reach,
 // 32-bit data format (the raw-buffer setting).

@@ -136,6 +136,8 @@ def test_long_query_tiles_come_first():
     (dict(geom=(8, 1, 128, 4, 10)), tsa.EUNSUPPORTED),
     (dict(geom=(8, 1, 128, 16, 0)), tsa.EINVAL),
     (dict(geom=(512, 1, 128, 16, 10)), tsa.EUNSUPPORTED),
+    # one page of all KV heads (Hkv * ps * d * 2 bytes) must stay below 2 GiB
+    (dict(geom=(65536, 65536, 128, 256, 10)), tsa.EUNSUPPORTED),
     (dict(pre=[-1]), tsa.EINVAL),
     (dict(suf=[-5]), tsa.EINVAL),
     (dict(stride=1), tsa.EINVAL),

@@ -8,12 +8,12 @@
 // layer-first page layout into a flat per-sequence view (Appendix C).
 //
 // Work unit: one workgroup per (logical page, sequence, KV head).  K page
-// rows are contiguous and move as 16-byte chunks; V page blocks are stored
-// tokens-innermost, so each thread reads 8 slots of one feature row with
-// one 16-byte load and scatters them to 8 output rows (a wave covers 64
-// consecutive features of one token per store, so stores stay coalesced).
-// Pool and output bytes stream through once: K copies and V loads are
-// non-temporal.
+// rows are contiguous and move as 16-byte chunks.  V page blocks are stored
+// tokens-innermost, so V is transposed through LDS: each thread reads 8
+// slots of one feature row with one 16-byte load and writes them into a
+// token-major LDS tile, then reads 8 consecutive features of one token and
+// writes them to the output row with one 16-byte store.  Pool and output
+// bytes stream through once: loads and stores are non-temporal.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -52,6 +52,11 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(PlanData p, const uint16
         __builtin_nontemporal_store(__builtin_nontemporal_load(src), dst);
     }
 
+    // V: page block [D][ps] -> LDS tile [ps][D] (token-major, rows padded by
+    // 4 bytes so the 2-byte column writes spread over the banks) -> output
+    // rows in 16-byte chunks.
+    extern __shared__ __attribute__((aligned(16))) char vt[];
+    constexpr int kRow = 2 * D + 4;
     const uint16_t* vpage = v_pool + (page * hkv + g) * (int64_t)D * ps;
     const int ngrp = (ntok + 7) >> 3;
     for (int c = threadIdx.x; c < ngrp * D; c += 256) {
@@ -64,8 +69,21 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(PlanData p, const uint16
         u.v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vpage + (int64_t)d * ps + s0));
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            if (s0 + e < ntok)
-                v_out[((out0 + s0 + e) * hkv + g) * D + d] = u.h[e];
+            *reinterpret_cast<uint16_t*>(vt + (s0 + e) * kRow + d * 2) = u.h[e];
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < ntok * CH; c += 256) {
+        const int sl = c / CH, col = c % CH;
+        union {
+            u32x4 v;
+            uint32_t w[4];
+        } u;
+        const uint32_t* src = reinterpret_cast<const uint32_t*>(vt + sl * kRow + col * 16);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            u.w[e] = src[e];
+        __builtin_nontemporal_store(
+            u.v, reinterpret_cast<u32x4*>(v_out + ((out0 + sl) * hkv + g) * D) + col);
     }
 }
 
@@ -91,11 +109,14 @@ extern "C" int talaria_sp_attn_gather_kv(const talaria_sp_plan* plan, const void
     auto vp = static_cast<const uint16_t*>(v_pool);
     auto ko = static_cast<uint16_t*>(k_out);
     auto vo = static_cast<uint16_t*>(v_out);
+    // LDS: one page of V, token-major, rows padded by 4 bytes (8-slot groups
+    // rounded up: a partial last group still writes whole groups).
+    const size_t lds = (size_t)((p->page_size + 7) & ~7) * (2 * p->head_dim + 4);
     if (p->head_dim == 128)
-        hipLaunchKernelGGL(gather_kv_kernel<128>, grid, dim3(256), 0, st, *p, kp, vp,
+        hipLaunchKernelGGL(gather_kv_kernel<128>, grid, dim3(256), lds, st, *p, kp, vp,
                            block_tables, ko, vo);
     else
-        hipLaunchKernelGGL(gather_kv_kernel<64>, grid, dim3(256), 0, st, *p, kp, vp,
+        hipLaunchKernelGGL(gather_kv_kernel<64>, grid, dim3(256), lds, st, *p, kp, vp,
                            block_tables, ko, vo);
     return launch_status("gather_kv");
 }

@@ -7,14 +7,15 @@
 // Work decomposition: the prefill plan's items (sequence, KV head, key-range
 // split); one workgroup of 4 waves per item.  The item's key range is cut
 // into 32-key steps dealt round-robin to the waves.  A wave streams a step's
-// K rows into its own LDS buffer with direct-to-LDS loads (each instruction
-// moves 1 KB of whole rows of one page), from where they are read in the row
-// order that makes S^T land in the PV B-operand layout; V feature rows go
-// straight to registers as 16-byte runs of 8 keys (tokens are innermost in V
-// pages, so each V instruction also reads 1 KB contiguous).  K buffers and V
-// registers are double-buffered: the next step's loads are in flight while
-// the current step computes.  Page numbers are wave-uniform scalar reads, so
-// no vector-memory wait is needed to form an address.  Each wave keeps
+// K rows into its own LDS buffer with the buffer form of the direct-to-LDS
+// load (each instruction moves 1 KB of whole rows of one page), from where
+// they are read in the row order that makes S^T land in the PV B-operand
+// layout; V feature rows go straight to registers as 16-byte runs of 8 keys
+// (tokens are innermost in V pages, so each V instruction also reads 1 KB
+// contiguous).  K buffers and V registers are double-buffered: the next
+// step's loads are in flight while the current step computes.  Page numbers
+// are wave-uniform scalar reads, made one step ahead of the loads that use
+// them, so no load waits on its own page lookup.  Each wave keeps
 // its own online-softmax state for the <= 32 query rows (one 32-row MFMA
 // block); the four states are merged through LDS at the end, and split items
 // go through the same log-sum-exp combine as the prefill.  Keys past the end
@@ -38,13 +39,41 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) const void gbl_void;
+typedef __attribute__((address_space(1))) const char gbl_char;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 constexpr int kWaves = 4;
 constexpr int kStep = 32;  // keys per wave step
+// Buffer descriptor of a page: no range clamp that a page offset could reach,
+// 32-bit data format (the raw-buffer setting).
+constexpr int kRsrcRecords = 0x7fffffff;
+constexpr int kRsrcFlags = 0x00020000;
+
+// s_waitcnt immediate that waits until at most N vector-memory operations of
+// the wave are outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
+// expcnt and lgkmcnt left at their maximum).
+template <int N>
+constexpr int vmcnt_only() {
+    static_assert(N >= 0 && N < 64, "vmcnt out of range");
+    return (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+
+// One 1 KB direct-to-LDS load: each lane moves the 16 bytes at base + off
+// into LDS bytes [16 lane, 16 lane + 16) of dst.
+__device__ __forceinline__ void load_lds_16(const gbl_char* base, uint32_t off, char* dst) {
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, kRsrcRecords, kRsrcFlags);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)dst, 16, off, 0, 0, 0);
+}
+
+// Waits until at most N vector-memory operations of the wave are outstanding
+// (a compiler-visible wait).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    __builtin_amdgcn_s_waitcnt(vmcnt_only<N>());
+}
 
 __device__ __forceinline__ int pi_row(int i) {
     return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1);
@@ -125,28 +154,38 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
     constexpr int KCH = D / 8;           // 16-byte chunks per K row
     char* const kbuf = reinterpret_cast<char*>(&s_k[wave][0][0]);
     const int last_krow_grp = ((kv_len - 1) / KRL) * KRL;
+    const uint32_t page_bytes = (uint32_t)(hkv * ps * D * 2);  // < 2^31 (planner)
+    const gbl_char* const kpool_g = (const gbl_char*)(const char*)k_pool + (int64_t)g * ps * D * 2;
     // Lane l fills LDS bytes [16 l, 16 l + 16) of a load: row l / KCH of the
     // load's row group, physical chunk l % KCH, which holds the row's logical
     // chunk (l % KCH) ^ kswz(row).
-    auto issue = [&](int k0, int b, u32x4 (&va)[2][DB]) {
+    uint32_t koff[KLOADS];
+#pragma unroll
+    for (int li = 0; li < KLOADS; ++li)
+        koff[li] = (uint32_t)(((lane / KCH) * D + ((lane % KCH) ^ kswz<D>(li * KRL + lane / KCH)) * 8) * 2);
+    // Pages of a step's four 8-key groups (keys k0, k0+8, k0+16, k0+24, each
+    // clamped to the last group holding a key).  A K load's rows and a V
+    // load's 8 keys lie in one such group, clamped the same way.
+    auto pages = [&](int k0, uint32_t (&pg)[4]) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            pg[j] = (uint32_t)bt_row[min(k0 + 8 * j, last_grp) >> shift];
+    };
+    auto issue = [&](int k0, int b, u32x4 (&va)[2][DB], const uint32_t (&pg)[4]) {
         char* kb = kbuf + b * (kStep * D * 2);
 #pragma unroll
         for (int li = 0; li < KLOADS; ++li) {
-            // Groups past the end re-read the last one (masked below).  The
-            // group's first key is wave-uniform, so its page is a scalar read.
+            // Groups past the end re-read the last one (masked below).
             const int key = min(k0 + li * KRL, last_krow_grp);
-            const int lc = (lane % KCH) ^ kswz<D>(li * KRL + lane / KCH);
-            const uint16_t* src =
-                k_pool +
-                (((int64_t)bt_row[key >> shift] * hkv + g) * ps + (key & (ps - 1)) + lane / KCH) * D +
-                lc * 8;
-            __builtin_amdgcn_global_load_lds((gbl_void*)src, (lds_void*)(kb + li * 1024), 16, 0, 0);
+            const gbl_char* base = kpool_g + (uint64_t)pg[(li * KRL) >> 3] * page_bytes +
+                                   (uint32_t)((key & (ps - 1)) * (D * 2));
+            load_lds_16(base, koff[li], kb + li * 1024);
         }
 #pragma unroll
         for (int ks2 = 0; ks2 < 2; ++ks2) {
-            // The two half-waves' 8-key groups: pages read as scalars.
+            // The two half-waves' 8-key groups.
             const int kg0 = min(k0 + 16 * ks2, last_grp), kg1 = min(k0 + 16 * ks2 + 8, last_grp);
-            const int32_t pg0 = bt_row[kg0 >> shift], pg1 = bt_row[kg1 >> shift];
+            const uint32_t pg0 = pg[2 * ks2], pg1 = pg[2 * ks2 + 1];
             const int kg = lh ? kg1 : kg0;
             const uint16_t* vb = v_pool + ((int64_t)(lh ? pg1 : pg0) * hkv + g) * D * ps +
                                  (kg & (ps - 1));
@@ -155,13 +194,30 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
                 va[ks2][db] = *reinterpret_cast<const u32x4*>(vb + (int64_t)(db * 32 + lq) * ps);
         }
     };
-    auto compute = [&](int k0, int b, u32x4 (&va)[2][DB]) {
+    // S^T = K Q^T over the step's 32 keys (K rows read in pi_row order).
+    auto qk = [&](int b) {
         const char* kb = kbuf + b * (kStep * D * 2);
-        // V slots past the end: zero, whatever they hold.
+        f32x16 sc = f32x16{};
+        const int row = pi_row(lq);
 #pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-            const int kg = min(k0 + 16 * ks2 + 8 * lh, last_grp);
-            if (kg + 8 > kv_len) {
+        for (int ks = 0; ks < KS; ++ks) {
+            const int lc = 2 * ks + lh;
+            const u32x4 a = *reinterpret_cast<const u32x4*>(kb + row * (2 * D) +
+                                                            ((lc ^ kswz<D>(row)) << 4));
+            sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), qf[ks], sc,
+                                                         0, 0, 0);
+        }
+        return sc;
+    };
+    // Softmax step and O^T += V^T P^T for the step at k0.
+    auto rest = [&](int k0, f32x16 sc, u32x4 (&va)[2][DB]) {
+        // V slots past the end: zero, whatever they hold.  Only the step
+        // holding the end needs it (a wave-uniform test); inside it the mask
+        // is applied branch-free.
+        if (k0 + kStep > kv_len) {
+#pragma unroll
+            for (int ks2 = 0; ks2 < 2; ++ks2) {
+                const int kg = min(k0 + 16 * ks2 + 8 * lh, last_grp);
 #pragma unroll
                 for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -170,19 +226,6 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
                                               (kg + e + 1 < kv_len ? 0xFFFF0000u : 0u);
                         va[ks2][db][e / 2] &= keep;
                     }
-            }
-        }
-        // S^T = K Q^T over 32 keys (K rows read in pi_row order).
-        f32x16 sc = f32x16{};
-        {
-            const int row = pi_row(lq);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int lc = 2 * ks + lh;
-                const u32x4 a = *reinterpret_cast<const u32x4*>(kb + row * (2 * D) +
-                                                                ((lc ^ kswz<D>(row)) << 4));
-                sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), qf[ks],
-                                                             sc, 0, 0, 0);
             }
         }
         // Keys outside this item's range (or past the end): -inf.
@@ -222,28 +265,43 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
                 o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va[ks2][db]),
                                                                 pf[ks2], o[db], 0, 0, 0);
     };
-    // One pipelined step on buffer b: issue the step after it into the other
-    // buffer, wait for this step's K (the loads still allowed in flight are
-    // this step's V loads and everything of the next step), compute.
+    // One pipelined step on buffer b: wait for this step's K, read it from
+    // LDS for S = K Q^T, then issue the step after it into the other buffer
+    // (so no LDS read runs while a load into LDS is in flight, which would
+    // make the compiler wait for every load), wait for this step's V and
+    // finish the step.
+    // The pages of the step after the next are read here too, while the
+    // current step computes.
     constexpr int kStride = kWaves * kStep;
     u32x4 va0[2][DB], va1[2][DB];
-    auto run = [&](int k0, int b, u32x4 (&va_this)[2][DB], u32x4 (&va_next)[2][DB]) {
+    uint32_t pga[4], pgb[4];
+    auto run = [&](int k0, int b, u32x4 (&va_this)[2][DB], u32x4 (&va_next)[2][DB],
+                   const uint32_t (&pg_next)[4], uint32_t (&pg_after)[4]) {
+        // The waits are compiler-visible (wait_vmem), so after the
+        // branches join the compiler knows this step's loads are complete on
+        // both paths and adds no drain of its own.
+        wait_vmem<2 * DB>();
+        const f32x16 sc = qk(b);
         if (k0 + kStride < key_hi) {
-            issue(k0 + kStride, b ^ 1, va_next);
-            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * DB + KLOADS + 2 * DB) : "memory");
+            issue(k0 + kStride, b ^ 1, va_next, pg_next);
+            pages(k0 + 2 * kStride, pg_after);
+            wait_vmem<KLOADS + 2 * DB>();
         } else {
-            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * DB) : "memory");
+            wait_vmem<0>();
         }
-        compute(k0, b, va_this);
+        rest(k0, sc, va_this);
     };
     int k0 = key_lo + wave * kStep;
-    if (k0 < key_hi)
-        issue(k0, 0, va0);
+    if (k0 < key_hi) {
+        pages(k0, pga);
+        issue(k0, 0, va0, pga);
+        pages(k0 + kStride, pgb);
+    }
     for (; k0 < key_hi; k0 += 2 * kStride) {
-        run(k0, 0, va0, va1);
+        run(k0, 0, va0, va1, pgb, pga);
         if (k0 + kStride >= key_hi)
             break;
-        run(k0 + kStride, 1, va1, va0);
+        run(k0 + kStride, 1, va1, va0, pga, pgb);
     }
     __syncthreads();  // every wave is done with its K buffers (s_o aliases them)
 

@@ -42,7 +42,7 @@ def random_case(seed):
     return wl, splits, decode
 
 
-@pytest.mark.parametrize("seed", range(32))
+@pytest.mark.parametrize("seed", range(128))
 def test_random_batch_matches_oracle(seed):
     import gpu_harness as h
     wl, splits, decode = random_case(seed)

@@ -795,7 +795,7 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
     float mx = -INFINITY;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
-    constexpr int KB = 8;
+    constexpr int KB = 16;
     for (int k0 = 0; k0 < n; k0 += KB) {
         float lk[KB];
         f32x4 v[KB];

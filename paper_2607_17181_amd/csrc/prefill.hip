@@ -764,8 +764,9 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
 // split query tiles are launched (blocks past a sequence's own tile count,
 // or of sequences without splits, exit at once): a grid over every work
 // item spent most of its time dispatching blocks with nothing to do.
-// Base-2 LSE merge in split order.
-template <int D>
+// Base-2 LSE merge in split order, KB splits per round of loads (8 for
+// plans with few splits, 16 for many-split plans such as a decode batch).
+template <int D, int KB>
 __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* __restrict__ part_o,
                                                       const float* __restrict__ part_lse,
                                                       uint16_t* __restrict__ out,
@@ -791,11 +792,11 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
     constexpr int64_t kStrideO = (int64_t)kRowsPerTile * D;
     // Online merge in split order, KB splits per round of loads (all issued
     // before any is used): the running maximum only grows, and the sums are
-    // rescaled when it does.
+    // rescaled when it does.  The merge order, and so every result bit, does
+    // not depend on KB.
     float mx = -INFINITY;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
-    constexpr int KB = 16;
     for (int k0 = 0; k0 < n; k0 += KB) {
         float lk[KB];
         f32x4 v[KB];
@@ -885,9 +886,10 @@ int launch_combine(const PlanData& p, const float* part_o, const float* part_lse
     // The grid covers only split query tiles: per sequence, as many tiles as
     // the longest split sequence has, and the rows of the tallest split tile
     // (a decode batch's split tiles hold `group` rows, not kRowsPerTile).
-    int32_t rows = 0, tiles = 0;
+    int32_t rows = 0, tiles = 0, max_splits = 0;
     for (int32_t b = 0; b < p.num_seqs; ++b)
         if (num_splits_of(p, b) > 1) {
+            max_splits = max_splits > num_splits_of(p, b) ? max_splits : num_splits_of(p, b);
             const int32_t t = p.seq[b].suffix_len < p.tile_tokens ? p.seq[b].suffix_len
                                                                   : p.tile_tokens;
             rows = rows > t * p.group ? rows : t * p.group;
@@ -896,14 +898,23 @@ int launch_combine(const PlanData& p, const float* part_o, const float* part_lse
         }
     if (rows == 0)
         return TALARIA_SP_OK;
+    const bool many = max_splits > 8;
     if (p.head_dim == 128) {
-        constexpr int RPB = 256 / (128 / 4);
-        hipLaunchKernelGGL(combine_kernel<128>, dim3(tiles, ceil_div(rows, RPB), p.num_seqs), dim3(256),
-                           0, st, p, part_o, part_lse, out, lse);
+        const dim3 grid(tiles, ceil_div(rows, 256 / (128 / 4)), p.num_seqs);
+        if (many)
+            hipLaunchKernelGGL((combine_kernel<128, 16>), grid, dim3(256), 0, st, p, part_o,
+                               part_lse, out, lse);
+        else
+            hipLaunchKernelGGL((combine_kernel<128, 8>), grid, dim3(256), 0, st, p, part_o,
+                               part_lse, out, lse);
     } else {
-        constexpr int RPB = 256 / (64 / 4);
-        hipLaunchKernelGGL(combine_kernel<64>, dim3(tiles, ceil_div(rows, RPB), p.num_seqs), dim3(256), 0,
-                           st, p, part_o, part_lse, out, lse);
+        const dim3 grid(tiles, ceil_div(rows, 256 / (64 / 4)), p.num_seqs);
+        if (many)
+            hipLaunchKernelGGL((combine_kernel<64, 16>), grid, dim3(256), 0, st, p, part_o,
+                               part_lse, out, lse);
+        else
+            hipLaunchKernelGGL((combine_kernel<64, 8>), grid, dim3(256), 0, st, p, part_o,
+                               part_lse, out, lse);
     }
     return launch_status("combine");
 }

@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--config", default="single",
                     choices=["tiny", "single", "ragged", "long", "cold"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-xcd-calibration", action="store_true",
+                    help="leave XCD placement off (plans run item i on workgroup i)")
     ap.add_argument("--cpu-rows", type=int, default=16384,
                     help="query rows of the workload the oracle baseline computes")
     ap.add_argument("--extra-json", default=None,
@@ -64,7 +66,7 @@ def parse():
     return ap.parse_args()
 
 
-def time_config(name, steps, warmup, torch, tsa, harness, workload):
+def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=True):
     """Time `steps` whole-path steps; return a dict of figures."""
     wl = workload.make_workload(name)
     db = harness.DeviceBatch(wl, fill=0)
@@ -77,6 +79,16 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload):
     plans0 = db.plans()
     workspaces = [tsa.workspace_tensor(sp) for sp in plans0]
     chunk_t = [db.chunk_tensors(c) for c in range(n_chunks)]
+
+    # Set-up: measure the XCD order on the first chunk (one ordinary prefill
+    # with per-workgroup timing); the plans made in the timed steps are
+    # placed by it.
+    xcd_order = None
+    if calibrate and tsa.plan_items(plans0[0]).shape[0] >= 8:
+        q, kn, vn, out, _, _ = chunk_t[0]
+        tsa.append_kv(plans0[0], kn, vn, db.k_pool, db.v_pool, db.bt)
+        xcd_order = tsa.calibrate_xcd(plans0[0], q, db.k_pool, db.v_pool, db.bt, out,
+                                      workspaces[0])
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * n_chunks + 1)]
           for _ in range(steps)]
@@ -133,6 +145,7 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload):
         "append_gbs": append_bytes / (append_avg * 1e-3) / 1e9,
         "plan_us": plan_s / steps * 1e6,
         "num_items": [int(tsa.plan_items(sp).shape[0]) for sp in plans0],
+        "xcd_order": xcd_order,
         "workspace_bytes": [sp.workspace_bytes for sp in plans0],
         "wl": wl,
         "db": db,
@@ -442,7 +455,8 @@ def main():
               flush=True)
         return
 
-    r = time_config(args.config, args.steps, args.warmup, torch, tsa, harness, workload)
+    r = time_config(args.config, args.steps, args.warmup, torch, tsa, harness, workload,
+                    calibrate=not args.no_xcd_calibration)
     wl = r.pop("wl")
     r.pop("db")
     achieved = r["prefill_tflops"]
@@ -472,6 +486,7 @@ def main():
         },
         "pct_bf16_peak": round(100 * r["tflops_step"] / PEAK_BF16_TFLOPS, 2),
         "ms_per_continuation": round(r["ms_per_step"] / wl.num_seqs, 4),
+        "xcd_order": r["xcd_order"],
         "breakdown_ms": {"plan_host": round(r["plan_us"] / 1e3, 4),
                          "append_kv": round(r["append_ms"], 4),
                          "prefill_call": round(r["prefill_call_ms"], 4)},

@@ -192,6 +192,43 @@ TALARIA_SP_API int talaria_sp_attn_gather_kv(const talaria_sp_plan* plan, const 
  * Returns the number of work items (>= 0) or a negative status. */
 TALARIA_SP_API int talaria_sp_attn_plan_items(const talaria_sp_plan* plan, int32_t* items, int32_t max_items);
 
+/* ---- XCD placement ------------------------------------------------------
+ *
+ * Workgroup i of a launch runs on XCD i % 8, and the XCDs of one MI355X
+ * differ in speed by several percent, steadily from launch to launch.  With
+ * one round of equal-cost items the slowest XCD therefore sets the end of
+ * the call.  Once an XCD order is set, every prefill plan made afterwards
+ * that is one round of at most 256 items (and not a decode batch) places
+ * its longest items on the fastest XCDs.  Placement only changes which
+ * compute unit runs an item: results are bit-identical with or without it.
+ *
+ * talaria_sp_attn_calibrate_xcd measures the order on the caller's own
+ * batch: it runs one prefill of `plan` (outputs land in out / workspace as
+ * for talaria_sp_attn_prefill with the default scale and no LSE) with each
+ * workgroup recording its XCD and main-loop time into `stamps` (device
+ * memory, 32 bytes per work item), synchronises `stream`, ranks the XCDs by
+ * mean time per key tile and sets the order (also written to `order`,
+ * int32[8], unless NULL).  It synchronises and copies to the host, so it
+ * belongs in set-up, not in the serving loop.  The plan needs at least 8
+ * work items and a timed item on every XCD (a full-GPU batch, e.g. one
+ * 25K-token continuation, is a good calibration batch).  Returns EINVAL,
+ * ENOSPACE (stamps too small) or EHIP as the other calls do.
+ *
+ * talaria_sp_set_xcd_order sets the order directly (order[g] = the XCD that
+ * takes the g-th longest block; a permutation of 0..7) or, with NULL,
+ * clears it.  talaria_sp_get_xcd_order copies the order into order[8] and
+ * returns 1, or returns 0 when none is set.  The order is process-wide;
+ * plans already made keep their placement.  Host only.
+ */
+TALARIA_SP_API int talaria_sp_attn_calibrate_xcd(const talaria_sp_plan* plan, const void* q,
+                                                 const void* k_pool, const void* v_pool,
+                                                 const int32_t* block_tables, void* out,
+                                                 void* workspace, size_t workspace_bytes,
+                                                 void* stamps, size_t stamps_bytes,
+                                                 int32_t* order, void* stream);
+TALARIA_SP_API int talaria_sp_set_xcd_order(const int32_t* order);
+TALARIA_SP_API int talaria_sp_get_xcd_order(int32_t* order);
+
 /* ---- HKVR page transfer (host KV registry restore / checkpoint) ----------
  *
  * A returning session's prefix may live in pinned host memory instead of the

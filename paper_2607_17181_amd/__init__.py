@@ -12,6 +12,8 @@ The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
     prefill(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)
     decode(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)   # S_b <= 1
     gather_kv(sp, k_pool, v_pool, block_tables, k_out, v_out)
+    calibrate_xcd(sp, q, k_pool, v_pool, block_tables, out, workspace)  # set-up: XCD order
+    set_xcd_order(order) / get_xcd_order()
     hkvr_restore(cache, slab, page_ids, k_cache, v_cache)       # host -> device pages
     hkvr_checkpoint(cache, k_cache, v_cache, page_ids, slab)    # device pages -> host
     stage_mark_dirty(chunks, used_pages, num_pages, page_bytes, dirty)
@@ -122,6 +124,13 @@ def library() -> ctypes.CDLL:
                                           ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_int64)]
         lib.talaria_sp_select.restype = ctypes.c_int
+        lib.talaria_sp_attn_calibrate_xcd.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p,
+                                                      sz, p, sz, p, p]
+        lib.talaria_sp_set_xcd_order.argtypes = [p]
+        lib.talaria_sp_get_xcd_order.argtypes = [p]
+        for f in (lib.talaria_sp_attn_calibrate_xcd, lib.talaria_sp_set_xcd_order,
+                  lib.talaria_sp_get_xcd_order):
+            f.restype = ctypes.c_int
         lib.talaria_sp_last_error.argtypes = []
         lib.talaria_sp_last_error.restype = ctypes.c_char_p
         _lib = lib
@@ -283,6 +292,51 @@ def decode(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspace
     """talaria_sp_attn_decode: one new token per sequence (suffix lengths <= 1)."""
     _attention_call(library().talaria_sp_attn_decode, sp, q, k_pool, v_pool, block_tables, out,
                     lse, workspace, sm_scale, stream)
+
+
+def calibrate_xcd(sp: SpPlan, q, k_pool, v_pool, block_tables, out, workspace=None,
+                  stream=None) -> list:
+    """talaria_sp_attn_calibrate_xcd: time one prefill of ``sp`` per XCD and set the
+    process-wide XCD order (fastest first), which plans made afterwards use for
+    placement.  Synchronises the stream; returns the order."""
+    torch = _torch()
+    g = sp.geom
+    kshape, vshape = _pool_shapes(sp)
+    qshape = (sp.total_tokens, g.num_q_heads, g.head_dim)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        if not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    n = max(int(plan_items(sp).shape[0]), 1)
+    stamps = torch.empty(4 * n, dtype=torch.int64, device=q.device)
+    order = (ctypes.c_int32 * 8)()
+    _check(library().talaria_sp_attn_calibrate_xcd(
+        ctypes.byref(sp.raw), _dev(q, qshape, "q"), _dev(k_pool, kshape, "k_pool"),
+        _dev(v_pool, vshape, "v_pool"),
+        _dev(block_tables, (sp.num_seqs, sp.max_pages_per_seq), "block_tables", bits16=False,
+             dtype=torch.int32),
+        _dev(out, qshape, "out"), ws_ptr, ws_bytes, stamps.data_ptr(), stamps.numel() * 8,
+        order, _stream(stream)))
+    return list(order)
+
+
+def set_xcd_order(order: Optional[Sequence[int]]) -> None:
+    """talaria_sp_set_xcd_order: order[g] = XCD that takes the g-th longest block of
+    items (a permutation of 0..7); None clears the order."""
+    if order is None:
+        _check(library().talaria_sp_set_xcd_order(None))
+        return
+    arr = (ctypes.c_int32 * 8)(*[int(x) for x in order]) if len(order) == 8 else None
+    if arr is None:
+        raise ValueError("order must have 8 entries")
+    _check(library().talaria_sp_set_xcd_order(arr))
+
+
+def get_xcd_order() -> Optional[list]:
+    """talaria_sp_get_xcd_order: the current XCD order, or None when none is set."""
+    arr = (ctypes.c_int32 * 8)()
+    return list(arr) if _check(library().talaria_sp_get_xcd_order(arr)) == 1 else None
 
 
 def gather_kv(sp: SpPlan, k_pool, v_pool, block_tables, k_out, v_out, stream=None) -> None:

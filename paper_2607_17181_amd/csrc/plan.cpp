@@ -22,6 +22,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 
@@ -75,6 +76,51 @@ int launch_status(const char* what) {
 using namespace tsp;
 
 extern "C" const char* talaria_sp_last_error(void) { return g_error; }
+
+namespace {
+
+// XCD order for placement, fastest XCD first (process-wide; see
+// talaria_sp_set_xcd_order).
+std::mutex g_xcd_mutex;
+bool g_xcd_set = false;
+int32_t g_xcd_order[tsp::kXcds];
+
+bool xcd_order_snapshot(int32_t* out) {
+    std::lock_guard<std::mutex> lock(g_xcd_mutex);
+    if (g_xcd_set)
+        memcpy(out, g_xcd_order, sizeof g_xcd_order);
+    return g_xcd_set;
+}
+
+}  // namespace
+
+extern "C" int talaria_sp_set_xcd_order(const int32_t* order) {
+    if (!order) {
+        std::lock_guard<std::mutex> lock(g_xcd_mutex);
+        g_xcd_set = false;
+        return TALARIA_SP_OK;
+    }
+    bool seen[kXcds] = {};
+    for (int g = 0; g < kXcds; ++g) {
+        if (order[g] < 0 || order[g] >= kXcds || seen[order[g]])
+            return fail(TALARIA_SP_EINVAL, "xcd order must be a permutation of 0..%d", kXcds - 1);
+        seen[order[g]] = true;
+    }
+    std::lock_guard<std::mutex> lock(g_xcd_mutex);
+    memcpy(g_xcd_order, order, sizeof g_xcd_order);
+    g_xcd_set = true;
+    return TALARIA_SP_OK;
+}
+
+extern "C" int talaria_sp_get_xcd_order(int32_t* order) {
+    if (!order)
+        return fail(TALARIA_SP_EINVAL, "order must not be NULL");
+    int32_t o[kXcds];
+    if (!xcd_order_snapshot(o))
+        return 0;
+    memcpy(order, o, sizeof o);
+    return 1;
+}
 
 extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seqs,
                                     const int32_t* prefix_lens, const int32_t* suffix_lens,
@@ -227,6 +273,41 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     p.seq[num_seqs].tok_off = (int32_t)tok;
     p.num_items = (int32_t)items;
     p.num_part_items = (int32_t)part_items;
+
+    // XCD placement.  Workgroup i of a launch runs on XCD i % kXcds, and
+    // XCDs of one part differ in speed by several percent, steadily.  Once an
+    // XCD order is set (fastest first, as talaria_sp_attn_calibrate_xcd
+    // measures it), a prefill plan that is one round of at most kMappedItems
+    // items ranks its items by key tiles, longest first, and deals them out
+    // in blocks: the fastest XCD takes the longest block, so the XCDs' last
+    // items end at about the same time.  Placement changes which compute
+    // unit runs an item, never what it computes.
+    int32_t order[kXcds];
+    if (!decode_batch && items > 0 && items <= kMappedItems && xcd_order_snapshot(order)) {
+        const int32_t n = (int32_t)items;
+        int32_t rank[kMappedItems], cost[kMappedItems];
+        uint8_t uses[kMappedItems] = {};
+        for (int32_t i = 0; i < n; ++i) {
+            const WorkItem w = decode_item(p, i);
+            cost[i] = w.tile_end - w.tile_begin;
+            rank[i] = i;
+        }
+        std::sort(rank, rank + n, [&](int32_t a, int32_t b) {
+            return cost[a] != cost[b] ? cost[a] > cost[b] : a < b;
+        });
+        int32_t next = 0;
+        for (int g = 0; g < kXcds; ++g) {
+            const int32_t x = order[g];
+            for (int32_t wg = x; wg < n; wg += kXcds) {
+                p.item_of_wg[wg] = (uint8_t)rank[next];
+                ++uses[rank[next++]];
+            }
+        }
+        for (int32_t i = 0; i < n; ++i)
+            if (uses[i] != 1)
+                return fail(TALARIA_SP_EINVAL, "internal error: XCD placement is not one-to-one");
+        p.wg_mapped = 1;
+    }
 
     const int64_t part_o = part_items * kRowsPerTile * (int64_t)d * 4;
     const int64_t part_lse = part_items * kRowsPerTile * 4;

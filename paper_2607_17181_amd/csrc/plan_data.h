@@ -18,12 +18,14 @@
 namespace tsp {
 
 constexpr uint32_t kPlanMagic = 0x54535041u;  // "TSPA"
-constexpr uint32_t kPlanVersion = 1;
+constexpr uint32_t kPlanVersion = 2;
 
 // Work decomposition of the prefill kernel.
 constexpr int kRowsPerTile = 256;   // query rows (token x head-in-group) per work item
 constexpr int kKeysPerTile = 64;    // keys per K/V tile staged in LDS
 constexpr int kMaxSplits = 64;      // key-range splits per query tile
+constexpr int kXcds = 8;            // XCDs; workgroup i of a launch runs on XCD i % 8
+constexpr int kMappedItems = 256;   // plans of at most this many items may be XCD-placed
 
 struct SeqDesc {
     int32_t prefix_len;  // P_b
@@ -54,6 +56,10 @@ struct PlanData {
     int32_t max_seq_pages;      // most logical pages any sequence holds
     int64_t ws_lse_offset;      // byte offset of partial LSE in the workspace
     int64_t ws_bytes;           // workspace bytes needed
+    int32_t wg_mapped;          // 1: prefill workgroup i runs item item_of_wg[i]
+    int32_t pad0;
+    uint64_t stamps;            // device address of per-workgroup timing records, or 0
+    uint8_t item_of_wg[kMappedItems];  // XCD placement (wg_mapped only)
     int32_t kv_off[TALARIA_SP_MAX_SEQS + 1];  // gather output row offsets
     SeqDesc seq[TALARIA_SP_MAX_SEQS + 1];     // entry num_seqs: sentinel
 };

@@ -48,6 +48,9 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "common.h"
 
 namespace tsp {
@@ -463,7 +466,9 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     static_assert(QB == 1 && G::NW == 8, "the ping-pong schedule needs 8 waves of 32 rows");
     __shared__ __attribute__((aligned(1024))) char smem[(kKStages + kVStages) * G::TILE_BYTES];
 
-    const WorkItem w = decode_item(p, blockIdx.x);
+    // Workgroup i runs on XCD i % 8; an XCD-placed plan names its item.
+    const WorkItem w =
+        decode_item(p, p.wg_mapped ? (int32_t)p.item_of_wg[blockIdx.x] : (int32_t)blockIdx.x);
     const SeqDesc s = p.seq[w.seq];
     const int Gq = p.group;
     const int lane = threadIdx.x & 63;
@@ -693,8 +698,17 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         }
     };
     const int split = tmask < tb ? tb : (tmask > te ? te : tmask);
+    // Calibration launches record the main loop's duration per workgroup.
+    const uint64_t loop_t0 = p.stamps ? __builtin_amdgcn_s_memrealtime() : 0;
     run(tb, split, NoMask{});
     run(split, te, WithMask{});
+    if (p.stamps && threadIdx.x == 0) {
+        uint64_t* rec = reinterpret_cast<uint64_t*>(p.stamps) + 4 * (uint64_t)blockIdx.x;
+        rec[0] = __builtin_amdgcn_s_getreg((3 << 11) | 20);  // XCC id (HW_REG_XCC_ID[3:0])
+        rec[1] = (uint64_t)(te - tb);
+        rec[2] = loop_t0;
+        rec[3] = __builtin_amdgcn_s_memrealtime();
+    }
 
     if (tb < te) {
         // Of this item's tiles only the last one can reach past the sequence's
@@ -923,15 +937,14 @@ int launch_combine(const PlanData& p, const float* part_o, const float* part_lse
 
 using namespace tsp;
 
-extern "C" int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const void* q,
-                                       const void* k_pool, const void* v_pool,
-                                       const int32_t* block_tables, float sm_scale, void* out,
-                                       float* lse, void* workspace, size_t workspace_bytes,
-                                       void* stream) {
-    int status;
-    const PlanData* p = checked_plan(plan, &status);
-    if (!p)
-        return status;
+namespace {
+
+// Argument checks and launch shared by the prefill call and the XCD
+// calibration call.
+int prefill_impl(const PlanData& pd, const void* q, const void* k_pool, const void* v_pool,
+                 const int32_t* block_tables, float sm_scale, void* out, float* lse,
+                 void* workspace, size_t workspace_bytes, void* stream) {
+    const PlanData* p = &pd;
     if (p->num_items == 0)
         return TALARIA_SP_OK;
     if (!q || !k_pool || !v_pool || !block_tables || !out)
@@ -955,4 +968,74 @@ extern "C" int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const void* 
     if (p->head_dim == 128)
         return launch_prefill<128>(*p, qq, kp, vp, block_tables, sm_scale, o, lse, ws, st);
     return launch_prefill<64>(*p, qq, kp, vp, block_tables, sm_scale, o, lse, ws, st);
+}
+
+}  // namespace
+
+extern "C" int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const void* q,
+                                       const void* k_pool, const void* v_pool,
+                                       const int32_t* block_tables, float sm_scale, void* out,
+                                       float* lse, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+    int status;
+    const PlanData* p = checked_plan(plan, &status);
+    if (!p)
+        return status;
+    return prefill_impl(*p, q, k_pool, v_pool, block_tables, sm_scale, out, lse, workspace,
+                        workspace_bytes, stream);
+}
+
+extern "C" int talaria_sp_attn_calibrate_xcd(const talaria_sp_plan* plan, const void* q,
+                                             const void* k_pool, const void* v_pool,
+                                             const int32_t* block_tables, void* out,
+                                             void* workspace, size_t workspace_bytes,
+                                             void* stamps, size_t stamps_bytes, int32_t* order,
+                                             void* stream) {
+    int status;
+    const PlanData* p = checked_plan(plan, &status);
+    if (!p)
+        return status;
+    const int32_t n = p->num_items;
+    if (n < kXcds)
+        return fail(TALARIA_SP_EINVAL, "calibrate_xcd: the plan has %d work items; at least "
+                    "%d (one per XCD) are needed", n, kXcds);
+    if (!stamps || stamps_bytes < (size_t)n * 32)
+        return fail(TALARIA_SP_ENOSPACE, "calibrate_xcd: stamps needs %lld bytes",
+                    (long long)n * 32);
+    PlanData c = *p;
+    c.wg_mapped = 0;
+    c.stamps = reinterpret_cast<uint64_t>(stamps);
+    status = prefill_impl(c, q, k_pool, v_pool, block_tables, 0.f, out, nullptr, workspace,
+                          workspace_bytes, stream);
+    if (status != TALARIA_SP_OK)
+        return status;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    std::vector<uint64_t> rec((size_t)n * 4);
+    hipError_t e = hipStreamSynchronize(st);
+    if (e == hipSuccess)
+        e = hipMemcpy(rec.data(), stamps, rec.size() * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess)
+        return fail(TALARIA_SP_EHIP, "calibrate_xcd: %s", hipGetErrorString(e));
+    // Mean main-loop time per key tile on each XCD (the real-time counter
+    // ticks at 100 MHz), then the XCDs from fastest to slowest.
+    double ns[kXcds] = {}, cnt[kXcds] = {};
+    for (int32_t i = 0; i < n; ++i) {
+        const uint64_t x = rec[4 * i] & 15, tiles = rec[4 * i + 1];
+        if (x < (uint64_t)kXcds && tiles > 0 && rec[4 * i + 3] >= rec[4 * i + 2]) {
+            ns[x] += 10.0 * (double)(rec[4 * i + 3] - rec[4 * i + 2]) / (double)tiles;
+            cnt[x] += 1.0;
+        }
+    }
+    int32_t ord[kXcds];
+    for (int x = 0; x < kXcds; ++x) {
+        if (cnt[x] == 0)
+            return fail(TALARIA_SP_EINVAL, "calibrate_xcd: no timed work item ran on XCD %d", x);
+        ns[x] /= cnt[x];
+        ord[x] = x;
+    }
+    std::stable_sort(ord, ord + kXcds, [&](int32_t a, int32_t b) { return ns[a] < ns[b]; });
+    status = talaria_sp_set_xcd_order(ord);
+    if (status == TALARIA_SP_OK && order)
+        memcpy(order, ord, sizeof ord);
+    return status;
 }

@@ -22,7 +22,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = tsa.library()
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 15
     for n in names:
         assert hasattr(lib, n), n
 
@@ -203,3 +203,56 @@ def test_decode_rejects_multi_token_plans_without_launching():
     rc = tsa.library().talaria_sp_attn_decode(ctypes.byref(sp.raw), fake, fake, fake, fake, 0.0,
                                               fake, None, None, 0, None)
     assert rc == tsa.EUNSUPPORTED
+
+
+@pytest.fixture
+def clear_xcd_order():
+    tsa.set_xcd_order(None)
+    yield
+    tsa.set_xcd_order(None)
+
+
+def test_xcd_order_is_validated_and_cleared(clear_xcd_order):
+    assert tsa.get_xcd_order() is None
+    tsa.set_xcd_order([6, 4, 0, 5, 2, 3, 7, 1])
+    assert tsa.get_xcd_order() == [6, 4, 0, 5, 2, 3, 7, 1]
+    for bad in ([0, 0, 1, 2, 3, 4, 5, 6], [0, 1, 2, 3, 4, 5, 6, 8], [-1, 1, 2, 3, 4, 5, 6, 7]):
+        with pytest.raises(tsa.TalariaError) as e:
+            tsa.set_xcd_order(bad)
+        assert e.value.status == tsa.EINVAL
+    assert tsa.get_xcd_order() == [6, 4, 0, 5, 2, 3, 7, 1]  # a rejected order changes nothing
+    tsa.set_xcd_order(None)
+    assert tsa.get_xcd_order() is None
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_placed_plans_keep_their_work_list(seed, clear_xcd_order):
+    """With an XCD order set, single-round plans are placed (the planner checks
+    internally that placement is one-to-one and fails the call otherwise); the
+    work list itself, and so coverage, is unchanged."""
+    rng = np.random.default_rng(900 + seed)
+    geom = _geom(pages=1 << 30)
+    n = int(rng.integers(1, 9))
+    pre = rng.integers(0, 30_000, size=n).tolist()
+    suf = rng.integers(1, 3_000, size=n).tolist()
+    stride = (max(p + s for p, s in zip(pre, suf)) + 15) // 16
+    base = tsa.plan_items(tsa.plan(geom, pre, suf, stride))
+    tsa.set_xcd_order(rng.permutation(8).tolist())
+    sp = tsa.plan(geom, pre, suf, stride)
+    check_coverage(sp, geom)
+    assert np.array_equal(tsa.plan_items(sp), base)
+
+
+def test_calibrate_rejects_small_plans_without_launching(clear_xcd_order):
+    sp = tsa.plan(_geom(), [100], [5], 16)  # one work item
+    fake = 0x1000
+    order = (ctypes.c_int32 * 8)()
+    rc = tsa.library().talaria_sp_attn_calibrate_xcd(ctypes.byref(sp.raw), fake, fake, fake, fake,
+                                                     fake, None, 0, fake, 1 << 20, order, None)
+    assert rc == tsa.EINVAL and "at least" in tsa.last_error()
+    sp = tsa.plan(_geom(), [25_000], [2_048], 1700)
+    rc = tsa.library().talaria_sp_attn_calibrate_xcd(ctypes.byref(sp.raw), fake, fake, fake, fake,
+                                                     fake, fake, sp.workspace_bytes, fake, 64,
+                                                     order, None)
+    assert rc == tsa.ENOSPACE
+    assert tsa.get_xcd_order() is None

@@ -322,11 +322,12 @@ TALARIA_SP_API int talaria_stage_gather(const talaria_stage_chunk* chunks, int32
 
 /* ---- SP batch selection (host) -------------------------------------------
  *
- * At an SP opportunity the scheduler admits a bounded batch of the eligible
- * continuations whose predicted prefill, restore and HBM costs fit what the
- * slot has left after protected decode; calls that do not fit stay queued
- * (Section 3.4).  talaria_sp_select scans candidates in queue order and
- * admits each one that still fits all bounds (first fit), skipping the rest.
+ * Each SP opportunity takes a bounded set of the waiting continuations,
+ * sized so that its predicted cost (attention time, page restore time,
+ * device pages) stays inside what the slot has left once decode is served;
+ * the others wait (Section 3.4).  talaria_sp_select scans candidates in
+ * queue order and admits each one that still fits all bounds (first fit),
+ * skipping the rest.
  *
  * Predicted cost of a candidate (host-resident prefixes are restored page
  * aligned, their partial last page recomputed with the suffix, Appendix B:

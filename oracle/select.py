@@ -1,11 +1,12 @@
 """CPU oracle for SP batch selection -- TEST INFRASTRUCTURE ONLY.
 
 Only the tests may import this module; the product path never does.
-Written from the paper's description (Section 3.4): at an SP opportunity the
-scheduler admits, from the eligible continuations, a bounded batch whose
-predicted prefill, restore and HBM costs fit the budget left after protected
-decode; calls that do not fit stay queued.  Reading taken: candidates in
-queue order, each admitted when the batch with it still fits (first fit).
+Written from Section 3.4's admission rule: each SP opportunity takes a
+bounded set of waiting continuations, sized so that their predicted cost
+(attention, page restore, device pages) stays within what the slot has left
+once decode is served; anything else waits for a later opportunity.  Reading
+taken: candidates in queue order, each admitted when the batch with it still
+fits (first fit).
 Host-resident prefixes are restored page aligned (Appendix B), the partial
 last page joining the recomputed tail.
 """

@@ -34,8 +34,8 @@ from typing import Optional, Sequence
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-# The in-tree build; TALARIA_SP_LIB may name another build of the same library.
-LIB_PATH = os.environ.get("TALARIA_SP_LIB") or os.path.join(_PKG, "libtalaria_sp_attn.so")
+# The in-tree build, and only that one.
+LIB_PATH = os.path.join(_PKG, "libtalaria_sp_attn.so")
 
 OK, EINVAL, EUNSUPPORTED, ENOSPACE, EHIP = 0, -1, -2, -3, -4
 MAX_SEQS = 128

@@ -30,6 +30,3 @@ int launch_combine(const PlanData& p, const float* part_o, const float* part_lse
 }  // namespace tsp
 #endif
 
-namespace tsp {
-
-}  // namespace tsp

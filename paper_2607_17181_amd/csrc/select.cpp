@@ -1,7 +1,8 @@
-// SP batch selection (host): at an SP opportunity the cold-pool scheduler
-// forms the eligible set of returning continuations and admits a bounded
-// batch whose predicted prefill, restore and HBM costs fit what is left of
-// the slot after protected decode; the rest stay queued (paper Section 3.4).
+// SP batch selection (host), after Section 3.4: at each SP opportunity a
+// bounded set of the waiting returning continuations is taken, sized so that
+// its predicted cost (attention time, page restore time, device pages) stays
+// inside what the slot has left once decode is served; the others wait for
+// a later opportunity.
 //
 // Rule: candidates are taken in queue (arrival) order; each is admitted if
 // the batch with it still fits every bound -- predicted time, free device

@@ -288,7 +288,38 @@ def pin_bad_page_id_rejected(lib=None):
     raise AssertionError("out-of-range page id was accepted")
 
 
+def pin_row_subset(lib=None):
+    """The row-subset mode (output k belongs to flat row rows[k] = token * Hq +
+    head) against brute force and, bit for bit, against the all-rows mode, on
+    a permutation of every row, an unsorted list with duplicates that crosses
+    sequences and heads, and a single row; for both the paged and the
+    contiguous entry point."""
+    wl, kp, vp = _case(20, Hq=4, Hkv=2, d=16, ps=4, pre=(9, 0, 14), suf=(5, 7, 3), num_pages=40)
+    o_all, lse_all, kp2, vp2 = _run_oracle(wl, kp, vp, lib)
+    bo, blse = brute_force(wl)
+    T, Hq, d = wl.q.shape
+    flat_o, flat_lse = o_all.reshape(T * Hq, d), lse_all.reshape(T * Hq)
+    bo, blse = bo.reshape(T * Hq, d), blse.reshape(T * Hq)
+    rng = np.random.default_rng(21)
+    lists = [rng.permutation(T * Hq),
+             np.array([T * Hq - 1, 0, 17, 17, 5, 44, 3, 17, 58, 1, 0, 29], dtype=np.int64),
+             np.array([33], dtype=np.int64)]
+    kc, vc = oracle.gather_kv(wl.prefix_lens, wl.suffix_lens, wl.block_tables, wl.page_size,
+                              kp2, vp2, lib_path=lib)
+    for i, rows in enumerate(lists):
+        o, lse = oracle.sp_attention(wl.prefix_lens, wl.suffix_lens, wl.block_tables,
+                                     wl.page_size, wl.q, kp2, vp2, rows=rows, lib_path=lib)
+        assert np.max(np.abs(o - bo[rows])) <= TOL, f"list {i}: rows differ from brute force"
+        assert np.max(np.abs(lse - blse[rows])) <= TOL, f"list {i}: lse differs from brute force"
+        assert np.array_equal(o, flat_o[rows]) and np.array_equal(lse, flat_lse[rows]), \
+            f"list {i}: rows mode differs from all-rows mode"
+        oc, lc = oracle.attention_contiguous(wl.prefix_lens, wl.suffix_lens, wl.q, kc, vc,
+                                             rows=rows, lib_path=lib)
+        assert np.array_equal(oc, o) and np.array_equal(lc, lse), \
+            f"list {i}: contiguous rows mode differs from paged rows mode"
+
+
 ALL_PINS = [pin_bruteforce, pin_torch_sdpa, pin_constant_v, pin_zero_q, pin_first_token,
             pin_dominant_logit, pin_paged_equals_contiguous, pin_page_permutation,
             pin_chunked_equals_oneshot, pin_gqa_identical_queries, pin_stale_slots_ignored,
-            pin_append_scatter, pin_gather, pin_bad_page_id_rejected]
+            pin_append_scatter, pin_gather, pin_bad_page_id_rejected, pin_row_subset]

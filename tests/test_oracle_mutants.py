@@ -36,6 +36,11 @@ MUTANTS = [
     ("gather_head_mixup", "int64_t dst = ((off + t) * Hkv + g) * d + e;",
      "int64_t dst = ((off + t) * Hkv + (Hkv - 1 - g)) * d + e;"),
     ("sign_flip_dot", "scores[j] = sigma * dot;", "scores[j] = -sigma * dot;"),
+    # Row-subset mode: the row list ignored, and output k written to slot r.
+    # The pin's first list is a permutation of every row, so the second
+    # mutant stays in bounds until that list's check fails.
+    ("rows_list_ignored", "int64_t r = rows ? rows[k] : k;", "int64_t r = k;"),
+    ("rows_output_slot", "o + k * d, lse + k);", "o + r * d, lse + r);"),
 ]
 
 

@@ -159,6 +159,31 @@ TALARIA_SP_API int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const vo
                             void* stream);
 
 /*
+ * Allocation-free prefill, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): talaria_sp_attn_prefill without the workspace argument.  Same
+ * plan, inputs, outputs, kernels and results (bit-identical to
+ * talaria_sp_attn_prefill on the same plan).  Split partials go to a
+ * scratch array inside the library instead: TALARIA_SP_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) of device memory on every GPU the library runs on, held until the
+ * process ends.  A plan whose workspace_bytes exceeds that returns
+ * TALARIA_SP_ENOSPACE before anything is launched.  The call allocates
+ * nothing; its first call on a device looks up that device's scratch
+ * address once (no allocation, no stream work).
+ *
+ * Every call on one GPU shares that GPU's scratch, and the scratch keeps the
+ * last call's contents: calls that overlap on one GPU (other streams, other
+ * threads) race and must be ordered by the caller.
+ */
+#define TALARIA_SP_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+TALARIA_SP_API int talaria_sp_attn_prefill_noalloc(const talaria_sp_plan* plan, const void* q,
+                                                   const void* k_pool, const void* v_pool,
+                                                   const int32_t* block_tables, float sm_scale,
+                                                   void* out, float* lse, void* stream);
+/* TALARIA_SP_NOALLOC_SCRATCH_BYTES as the built library has it. */
+TALARIA_SP_API size_t talaria_sp_attn_noalloc_scratch_bytes(void);
+
+/*
  * Decode: the S_b = 1 case of prefill -- each sequence's one new token (at
  * position P_b, its K/V appended first) attends to keys 0 .. P_b -- with a
  * kernel built for it: the D phase that resumes after an SP batch (Section

@@ -10,6 +10,7 @@ The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
     sp = plan(geom, prefix_lens, suffix_lens, max_pages_per_seq)
     append_kv(sp, k_new, v_new, k_pool, v_pool, block_tables)
     prefill(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)
+    prefill_noalloc(sp, q, k_pool, v_pool, block_tables, out, lse)     # no workspace
     decode(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)   # S_b <= 1
     gather_kv(sp, k_pool, v_pool, block_tables, k_out, v_out)
     calibrate_xcd(sp, q, k_pool, v_pool, block_tables, out, workspace)  # set-up: XCD order
@@ -101,6 +102,11 @@ def library() -> ctypes.CDLL:
         lib.talaria_sp_attn_append_kv.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p]
         lib.talaria_sp_attn_prefill.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
                                                 ctypes.c_float, p, p, p, sz, p]
+        lib.talaria_sp_attn_prefill_noalloc.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
+                                                        ctypes.c_float, p, p, p]
+        lib.talaria_sp_attn_prefill_noalloc.restype = ctypes.c_int
+        lib.talaria_sp_attn_noalloc_scratch_bytes.argtypes = []
+        lib.talaria_sp_attn_noalloc_scratch_bytes.restype = ctypes.c_size_t
         lib.talaria_sp_attn_gather_kv.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p]
         lib.talaria_sp_attn_decode.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
                                                ctypes.c_float, p, p, p, sz, p]
@@ -285,6 +291,31 @@ def prefill(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspac
     """talaria_sp_attn_prefill: causal SP attention into ``out`` (and ``lse``)."""
     _attention_call(library().talaria_sp_attn_prefill, sp, q, k_pool, v_pool, block_tables, out,
                     lse, workspace, sm_scale, stream)
+
+
+def prefill_noalloc(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None,
+                    sm_scale: float = 0.0, stream=None) -> None:
+    """talaria_sp_attn_prefill_noalloc: prefill with the library's own scratch in
+    place of a workspace (allocates nothing; overlapping calls on one GPU race)."""
+    torch = _torch()
+    g = sp.geom
+    kshape, vshape = _pool_shapes(sp)
+    qshape = (sp.total_tokens, g.num_q_heads, g.head_dim)
+    lse_ptr = None
+    if lse is not None:
+        lse_ptr = _dev(lse, (sp.total_tokens, g.num_q_heads), "lse", bits16=False,
+                       dtype=torch.float32)
+    args = (_dev(q, qshape, "q"), _dev(k_pool, kshape, "k_pool"), _dev(v_pool, vshape, "v_pool"),
+            _dev(block_tables, (sp.num_seqs, sp.max_pages_per_seq), "block_tables",
+                 bits16=False, dtype=torch.int32))
+    _check(library().talaria_sp_attn_prefill_noalloc(ctypes.byref(sp.raw), *args,
+                                                     float(sm_scale), _dev(out, qshape, "out"),
+                                                     lse_ptr, _stream(stream)))
+
+
+def noalloc_scratch_bytes() -> int:
+    """Bytes of per-GPU scratch behind prefill_noalloc."""
+    return int(library().talaria_sp_attn_noalloc_scratch_bytes())
 
 
 def decode(sp: SpPlan, q, k_pool, v_pool, block_tables, out, lse=None, workspace=None,

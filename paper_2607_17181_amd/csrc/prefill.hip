@@ -49,6 +49,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "common.h"
@@ -983,6 +984,86 @@ extern "C" int talaria_sp_attn_prefill(const talaria_sp_plan* plan, const void* 
         return status;
     return prefill_impl(*p, q, k_pool, v_pool, block_tables, sm_scale, out, lse, workspace,
                         workspace_bytes, stream);
+}
+
+// ---- Allocation-free prefill ---------------------------------------------
+//
+// Split partials of talaria_sp_attn_prefill_noalloc go to this array instead
+// of a caller workspace.  Every GPU the library runs on holds its own copy
+// for the life of the process.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is looked up once per
+// device (hipGetSymbolAddress, that device current) and only that address is
+// passed to kernels.
+constexpr size_t kScratchBytes = TALARIA_SP_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on the device that owns `stream`.
+int scratch_for_stream(hipStream_t stream, void** out) {
+    int dev = -1;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess)
+        return fail(TALARIA_SP_EHIP, "prefill_noalloc: hipStreamGetDevice: %s",
+                    hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(TALARIA_SP_EUNSUPPORTED, "prefill_noalloc: device %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        int cur = -1;
+        e = hipGetDevice(&cur);
+        if (e == hipSuccess && cur != dev)
+            e = hipSetDevice(dev);
+        void* ptr = nullptr;
+        if (e == hipSuccess)
+            e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur >= 0 && cur != dev) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess)
+                e = e2;
+        }
+        if (e != hipSuccess || !ptr)
+            return fail(TALARIA_SP_EHIP, "prefill_noalloc: scratch address on device %d: %s",
+                        dev, hipGetErrorString(e));
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return TALARIA_SP_OK;
+}
+
+}  // namespace
+
+extern "C" size_t talaria_sp_attn_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+extern "C" int talaria_sp_attn_prefill_noalloc(const talaria_sp_plan* plan, const void* q,
+                                               const void* k_pool, const void* v_pool,
+                                               const int32_t* block_tables, float sm_scale,
+                                               void* out, float* lse, void* stream) {
+    int status;
+    const PlanData* p = checked_plan(plan, &status);
+    if (!p)
+        return status;
+    if ((size_t)p->ws_bytes > kScratchBytes)
+        return fail(TALARIA_SP_ENOSPACE, "prefill_noalloc: the plan needs %lld bytes of "
+                    "scratch, the library holds %zu per GPU; use talaria_sp_attn_prefill with "
+                    "a workspace", (long long)p->ws_bytes, kScratchBytes);
+    if (p->num_items == 0)
+        return TALARIA_SP_OK;
+    if (!q || !k_pool || !v_pool || !block_tables || !out)
+        return fail(TALARIA_SP_EINVAL, "prefill_noalloc: q, k_pool, v_pool, block_tables and "
+                    "out must not be NULL");
+    void* ws = nullptr;
+    if (p->ws_bytes > 0) {
+        status = scratch_for_stream(reinterpret_cast<hipStream_t>(stream), &ws);
+        if (status != TALARIA_SP_OK)
+            return status;
+    }
+    return prefill_impl(*p, q, k_pool, v_pool, block_tables, sm_scale, out, lse, ws,
+                        kScratchBytes, stream);
 }
 
 extern "C" int talaria_sp_attn_calibrate_xcd(const talaria_sp_plan* plan, const void* q,

@@ -66,3 +66,21 @@ def test_stage_gather_argument_checks():
     # misaligned regions are rejected before any launch
     assert f(BAD, 2, BAD, BAD, BAD, 16, aligned, aligned, 16, NULL) == tsa.EINVAL
     assert "aligned" in tsa.last_error()
+
+
+def test_prefill_noalloc_rejects_plans_beyond_its_scratch():
+    """A plan whose workspace exceeds the per-GPU scratch is ENOSPACE before any
+    pointer is looked at or anything is launched; a plan that fits passes the
+    size check (and then stops at the NULL-pointer check)."""
+    lib = tsa.library()
+    assert tsa.noalloc_scratch_bytes() == 64 << 20
+    geom = tsa.make_geom(8, 1, 128, 16, 1000)
+    big = tsa.plan(geom, [5000], [256], 400, kv_splits=64)   # 8 query tiles x 64 splits
+    assert big.workspace_bytes > tsa.noalloc_scratch_bytes()
+    f = lib.talaria_sp_attn_prefill_noalloc
+    assert f(ctypes.byref(big.raw), BAD, BAD, BAD, BAD, 0.0, BAD, NULL, NULL) == tsa.ENOSPACE
+    assert "scratch" in tsa.last_error()
+    small = tsa.plan(geom, [5000], [256], 400, kv_splits=4)
+    assert 0 < small.workspace_bytes <= tsa.noalloc_scratch_bytes()
+    assert f(ctypes.byref(small.raw), NULL, BAD, BAD, BAD, 0.0, BAD, NULL, NULL) == tsa.EINVAL
+    assert f(None, BAD, BAD, BAD, BAD, 0.0, BAD, NULL, NULL) == tsa.EINVAL

@@ -89,7 +89,11 @@ typedef struct {
 } talaria_sp_plan;
 
 /*
- * Plan one SP batch (host only; touches no device state).
+ * Plan one SP batch (host only; touches no device state).  The batch is the
+ * bounded set of continuations that one SP opportunity admits (Section 3.4);
+ * each brings its committed prefix length (the device-resident KV of Section
+ * 4.1) and its new-token count, and the batch's prefill is the T_pf of that
+ * opportunity.
  *
  * geom                 pool geometry (host pointer).
  * num_seqs             sequences in the batch, 0 .. TALARIA_SP_MAX_SEQS.
@@ -113,6 +117,26 @@ TALARIA_SP_API int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num
                          const int32_t* prefix_lens, const int32_t* suffix_lens,
                          int32_t max_pages_per_seq, int32_t kv_splits,
                          size_t* workspace_bytes, talaria_sp_plan* plan);
+
+/*
+ * Opt-in host validation of block tables (for debugging and for callers that
+ * keep a host copy of their tables; host only, nothing is launched).  The
+ * kernels trust the tables: an id outside the pool is an out-of-bounds
+ * device access, and two sequences appending into one page corrupt each
+ * other.  host_block_tables is the host image of the block_tables the
+ * device calls take, int32[num_seqs][max_pages_per_seq].  For every
+ * sequence b and logical page p < ceil((P_b + S_b) / page_size) (the
+ * entries the calls read) it returns TALARIA_SP_EINVAL, naming the first
+ * offending entry, when:
+ *   - the id is outside [0, num_pages);
+ *   - the sequence names one physical page at two logical positions;
+ *   - a page that append writes (one holding some position
+ *     P_b .. P_b + S_b - 1) is named by any other entry of the batch.
+ * Pages that only hold cached prefix positions may be shared between
+ * sequences (read-only).  Entries past a sequence's last page are ignored.
+ */
+TALARIA_SP_API int talaria_sp_attn_check_tables(const talaria_sp_plan* plan,
+                                                const int32_t* host_block_tables);
 
 /*
  * Append: write the K and V rows of every new token into its pool slot

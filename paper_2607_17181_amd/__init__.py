@@ -8,6 +8,7 @@ library has not been built, every call raises.
 The calls mirror the C ABI in ``include/talaria_sp_attn.h``:
 
     sp = plan(geom, prefix_lens, suffix_lens, max_pages_per_seq)
+    check_tables(sp, host_block_tables)                               # opt-in, host only
     append_kv(sp, k_new, v_new, k_pool, v_pool, block_tables)
     prefill(sp, q, k_pool, v_pool, block_tables, out, lse, workspace)
     prefill_noalloc(sp, q, k_pool, v_pool, block_tables, out, lse)     # no workspace
@@ -107,6 +108,8 @@ def library() -> ctypes.CDLL:
         lib.talaria_sp_attn_prefill_noalloc.restype = ctypes.c_int
         lib.talaria_sp_attn_noalloc_scratch_bytes.argtypes = []
         lib.talaria_sp_attn_noalloc_scratch_bytes.restype = ctypes.c_size_t
+        lib.talaria_sp_attn_check_tables.argtypes = [ctypes.POINTER(_RawPlan), p]
+        lib.talaria_sp_attn_check_tables.restype = ctypes.c_int
         lib.talaria_sp_attn_gather_kv.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p, p, p]
         lib.talaria_sp_attn_decode.argtypes = [ctypes.POINTER(_RawPlan), p, p, p, p,
                                                ctypes.c_float, p, p, p, sz, p]
@@ -197,6 +200,18 @@ def plan(geom: Geom, prefix_lens: Sequence[int], suffix_lens: Sequence[int],
                                           int(max_pages_per_seq), int(kv_splits),
                                           ctypes.byref(ws), ctypes.byref(raw)))
     return SpPlan(raw, geom, pre.copy(), suf.copy(), int(max_pages_per_seq), int(ws.value))
+
+
+def check_tables(sp: SpPlan, host_block_tables) -> None:
+    """talaria_sp_attn_check_tables: validate a host copy of the block tables
+    (ids in range, no page twice in one sequence, appended pages exclusive);
+    raises TalariaError(EINVAL) naming the first bad entry."""
+    bt = np.ascontiguousarray(host_block_tables, dtype=np.int32)
+    if bt.shape != (sp.num_seqs, sp.max_pages_per_seq):
+        raise ValueError(f"block tables have shape {bt.shape}, expected "
+                         f"{(sp.num_seqs, sp.max_pages_per_seq)}")
+    _check(library().talaria_sp_attn_check_tables(ctypes.byref(sp.raw),
+                                                  bt.ctypes.data if bt.size else None))
 
 
 def plan_items(sp: SpPlan) -> np.ndarray:

@@ -23,6 +23,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <vector>
 
 #include "common.h"
 
@@ -317,6 +318,50 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     memset(plan, 0, sizeof *plan);
     memcpy(plan, &p, sizeof p);
     *workspace_bytes = (size_t)p.ws_bytes;
+    return TALARIA_SP_OK;
+}
+
+extern "C" int talaria_sp_attn_check_tables(const talaria_sp_plan* plan,
+                                            const int32_t* host_block_tables) {
+    int status;
+    const PlanData* p = checked_plan(plan, &status);
+    if (!p)
+        return status;
+    if (p->num_seqs > 0 && !host_block_tables)
+        return fail(TALARIA_SP_EINVAL, "check_tables: host_block_tables is NULL");
+    // last[page]: the last sequence that named the page (-1: none yet).
+    std::vector<int32_t> last((size_t)p->num_pages, -1);
+    std::vector<uint8_t> written((size_t)p->num_pages, 0);
+    // Pass 1: range, duplicates inside one sequence, and the written pages.
+    for (int32_t b = 0; b < p->num_seqs; ++b) {
+        const int64_t P = p->seq[b].prefix_len, S = p->seq[b].suffix_len;
+        const int64_t pages = (P + S + p->page_size - 1) >> p->page_shift;
+        const int32_t* row = host_block_tables + (int64_t)b * p->bt_stride;
+        for (int64_t lp = 0; lp < pages; ++lp) {
+            const int32_t id = row[lp];
+            if (id < 0 || id >= p->num_pages)
+                return fail(TALARIA_SP_EINVAL, "check_tables: sequence %d, logical page %lld: "
+                            "id %d outside [0, %d)", b, (long long)lp, id, p->num_pages);
+            if (last[id] == b)
+                return fail(TALARIA_SP_EINVAL, "check_tables: sequence %d names page %d at two "
+                            "logical positions (second at %lld)", b, id, (long long)lp);
+            last[id] = b;
+            if (S > 0 && lp >= (P >> p->page_shift) && lp <= ((P + S - 1) >> p->page_shift))
+                written[id] = 1;
+        }
+    }
+    // Pass 2: a written page must be named exactly once in the whole batch.
+    std::vector<int32_t> count((size_t)p->num_pages, 0);
+    for (int32_t b = 0; b < p->num_seqs; ++b) {
+        const int64_t P = p->seq[b].prefix_len, S = p->seq[b].suffix_len;
+        const int64_t pages = (P + S + p->page_size - 1) >> p->page_shift;
+        const int32_t* row = host_block_tables + (int64_t)b * p->bt_stride;
+        for (int64_t lp = 0; lp < pages; ++lp)
+            if (written[row[lp]] && ++count[row[lp]] > 1)
+                return fail(TALARIA_SP_EINVAL, "check_tables: page %d receives appended tokens "
+                            "and is also named by sequence %d, logical page %lld", row[lp], b,
+                            (long long)lp);
+    }
     return TALARIA_SP_OK;
 }
 

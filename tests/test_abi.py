@@ -22,7 +22,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = tsa.library()
     names = declared_functions()
-    assert len(names) == 17
+    assert len(names) == 18
     for n in names:
         assert hasattr(lib, n), n
 
@@ -256,3 +256,42 @@ def test_calibrate_rejects_small_plans_without_launching(clear_xcd_order):
                                                      order, None)
     assert rc == tsa.ENOSPACE
     assert tsa.get_xcd_order() is None
+
+
+def test_check_tables_accepts_generated_tables_and_rejects_bad_ones():
+    """The opt-in host check of block tables: the generator's tables pass
+    (prefix pages shared read-only between sequences pass too), and each
+    kind of bad entry is EINVAL with a message naming it."""
+    from workload import workload_from_lengths
+    wl = workload_from_lengths("tables", 3, num_q_heads=8, num_kv_heads=1, head_dim=64,
+                               page_size=16, num_pages=200, prefix_lens=[40, 0, 100],
+                               suffix_lens=[30, 20, 0], extra_pages_per_seq=2)
+    geom = tsa.make_geom(8, 1, 64, 16, 200)
+    sp = tsa.plan(geom, wl.prefix_lens, wl.suffix_lens, wl.max_pages_per_seq)
+    bt = wl.block_tables.copy()
+    tsa.check_tables(sp, bt)                       # as generated
+    junk = bt.copy()
+    junk[0, 5:] = 10**6                            # past the last page: never read
+    tsa.check_tables(sp, junk)
+    shared = bt.copy()
+    shared[2, 0] = bt[0, 0]                        # prefix page 0 of seq 0 (read-only) shared
+    tsa.check_tables(sp, shared)
+
+    def rejected(table, words):
+        with pytest.raises(tsa.TalariaError) as e:
+            tsa.check_tables(sp, table)
+        assert e.value.status == tsa.EINVAL
+        for w in words:
+            assert w in str(e.value)
+
+    bad = bt.copy(); bad[1, 1] = 200
+    rejected(bad, ["outside", "sequence 1"])
+    bad = bt.copy(); bad[2, 3] = -1
+    rejected(bad, ["outside", "sequence 2"])
+    bad = bt.copy(); bad[2, 4] = bt[2, 1]
+    rejected(bad, ["two logical positions"])
+    bad = bt.copy(); bad[2, 6] = bt[0, 3]          # seq 0's page 3 receives appended tokens
+    rejected(bad, ["appended"])
+    bad = bt.copy(); bad[0, 4] = bt[1, 0]          # seq 1 appends into its page 0
+    rejected(bad, ["appended"])
+    assert tsa.library().talaria_sp_attn_check_tables(ctypes.byref(sp.raw), None) == tsa.EINVAL

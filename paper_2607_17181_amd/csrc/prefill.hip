@@ -511,19 +511,19 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     // Load schedule.  In iteration t every wave issues its share of
     // K(t + kd) and V(t + vd), kd = 3 / vd = 2, at the start of the
     // iteration, which in both groups falls between barriers t-1 and t.  The
-    // prologue loads the tiles the first iterations need.  Loads are
-    // unconditional: a tile past the end reads the sequence's last page into
-    // a ring slot nobody reads.
+    // prologue loads the tiles the first iterations need.  No tile at or past
+    // te is loaded, so the workgroup never ends with a direct-to-LDS load in
+    // flight.
     const bool group_b = wave >= G::NW / 2;
     constexpr int kd = 3, vd = 2;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-        if (k < kd)
+        if (k < kd && tb + k < te)
             ld.issue_k(kbuf(tb + k), (tb + k) * kKeysPerTile,
                        c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
 #pragma unroll
     for (int k = 0; k < 3; ++k)
-        if (k < vd)
+        if (k < vd && tb + k < te)
             ld.issue_v(vbuf(tb + k), (tb + k) * kKeysPerTile,
                        c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
     uint32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
@@ -606,8 +606,15 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     // K(t+kd), v_rd holds V(t-1), v_wr receives V(t+vd).
     uint32_t k_rd = kslot(tb + 1), k_wr = kslot(tb + kd);
     uint32_t v_rd = vslot(tb - 1 + kVStages), v_wr = vslot(tb + vd);
-    auto sync_point = [&]() {
-        wait_vmem_n<2 * G::LOADS>();
+    // Loads for tiles at or past te are not issued, so in the last kd
+    // iterations fewer than 2 * LOADS loads are younger than the ones a
+    // barrier must see; there it waits for every load.  The loop therefore
+    // ends with no load in flight.
+    auto sync_point = [&](int t) {
+        if (t + kd < te)
+            wait_vmem_n<2 * G::LOADS>();
+        else
+            wait_vmem_all();
         lds_barrier();
     };
     auto iteration = [&](int t, auto mask_tag, const bf16x8 (&pf)[QB][4],
@@ -622,8 +629,10 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         float an[QB];
         // This iteration's tile loads, issued before the softmax so that the
         // MFMA phase holds only operand reads and MFMAs.
-        ld.issue_k(smem + k_wr, (uint32_t)(t + kd) * kKeysPerTile, pgk_next, c);
-        ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
+        if (t + kd < te)
+            ld.issue_k(smem + k_wr, (uint32_t)(t + kd) * kKeysPerTile, pgk_next, c);
+        if (t + vd < te)
+            ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
         bool rn = false;
         if (MASK || !softmax_fast<QB>(sc, pn, m_run, l_run, scale))
             rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile, qpos,
@@ -639,7 +648,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         }
         asm volatile("" ::"s"(pk), "s"(pv));
         if (group_b)
-            sync_point();
+            sync_point(t);
         __builtin_amdgcn_sched_barrier(0);
         // The MFMA phase runs at raised wave priority: its SIMD partner is in
         // its softmax, and without this the partner's VALU stream (an older
@@ -653,7 +662,8 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
                     o[qb][db] *= alpha[qb];
         }
         // MFMA phase, unconditional: P(tb-1) = 0 over a zeroed V stage, and
-        // S(te) comes from a stale slot and is never used.
+        // S(te) comes from a slot K(te) was never loaded into and is never
+        // used.
         pv_tile<D, SPAN, QB>(o, smem + v_rd, pf, oo);
         qk_tile<D, SPAN, QB>(sc, smem + k_rd, qf, oo);
         // Operand reads run four ahead of the MFMAs that use them, across the
@@ -677,7 +687,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
             alpha[qb] = an[qb];
         resc = rn;
         if (!group_b)
-            sync_point();
+            sync_point(t);
     };
 
     // P alternates between two register sets, two iterations per loop trip,

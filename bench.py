@@ -10,13 +10,19 @@ Workload: one continuation with a 25,000-token cached prefix and 2,048 new
 tokens, Hq=8 / Hkv=1 / head_dim=128 (one TP=8 rank's head share of a
 235B-class GQA model), page size 16, pages shuffled in a 100K-page pool.
 
-Prints ONE JSON line.  Extra figures (per-kernel times, other configs,
-standalone append/gather bandwidth) go to --extra-json when given.
+Prints ONE JSON line: the single continuation's throughput, with HIP-event
+step and prefill-call distributions (mean, nearest-rank p50 / p5 / p95), the
+prefill call's roofline, the CPU oracle timed beside it over all 16,384 query
+rows, and the parity of the timed GPU output against those rows; under
+"configs", the tiny, ragged, long and cold workloads timed the same way, each
+with the oracle's speed and parity on a seeded row sample.  Extra figures
+(per-kernel times, standalone append/gather bandwidth) go to --extra-json.
 """
 from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -28,6 +34,17 @@ sys.path.insert(0, HERE)
 sys.path.insert(0, os.path.join(HERE, "tests"))
 
 METRIC = "SP prefill attention TFLOP/s (% bf16 MFMA peak); ms per 25K-prefix continuation"
+WORKLOADS = {
+    "tiny": "tiny: 1 sequence, P=256 + S=64, Hq=2 Hkv=1 d=64, page 16, 64-page pool",
+    "single": "single continuation: P=25,000 cached + S=2,048 new tokens, Hq=8 Hkv=1 d=128, "
+              "page 16, shuffled 100K-page pool",
+    "ragged": "ragged SP batch: 16 continuations, P lognormal (median 25K, p95 105K, cap 128K), "
+              "S uniform 512-4096, Hq=8 Hkv=1 d=128, page 16, 300K-page pool",
+    "long": "long context: P=105,000 + S=8,192 as 4 chunked-prefill chunks of 2,048, "
+            "Hq=8 Hkv=1 d=128, page 16, 100K-page pool",
+    "cold": "cold recompute: 4 sequences, P=0 + S=25,000, Hq=8 Hkv=1 d=128, page 16, "
+            "100K-page pool",
+}
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
@@ -46,8 +63,13 @@ def parse():
                     help="query rows of the workload the oracle baseline computes")
     ap.add_argument("--extra-json", default=None,
                     help="write per-kernel / per-config figures to this file")
-    ap.add_argument("--all-configs", action="store_true",
-                    help="with --extra-json: also time every other config")
+    ap.add_argument("--no-extra-configs", action="store_true",
+                    help="time only --config (by default tiny, ragged, long and cold are also "
+                         "timed and reported under \"configs\")")
+    ap.add_argument("--extra-steps", type=int, default=20,
+                    help="timed steps for each of the other configs")
+    ap.add_argument("--extra-rows", type=int, default=4096,
+                    help="seeded query rows the oracle computes for each of the other configs")
     ap.add_argument("--hbm-sweep", action="store_true",
                     help="only time append_kv / gather_kv on 0.1-2 GB batches (cache flushed) "
                          "and print one JSON line")
@@ -64,6 +86,19 @@ def parse():
                     help="only run a plain device-to-device copy of MIB MiB three times "
                          "(reference for the HBM traffic counters) and exit")
     return ap.parse_args()
+
+
+def nearest_rank(values, q):
+    """p_q of `values` by the nearest-rank definition the paper's evaluation
+    uses (Section 5.1): the observation at rank ceil(q N / 100), 1-based."""
+    v = sorted(values)
+    return float(v[max(1, math.ceil(q * len(v) / 100)) - 1])
+
+
+def dist(values):
+    """Mean, nearest-rank median / p5 / p95 of a list of milliseconds."""
+    return {"mean": round(float(np.mean(values)), 4), "p50": round(nearest_rank(values, 50), 4),
+            "p5": round(nearest_rank(values, 5), 4), "p95": round(nearest_rank(values, 95), 4)}
 
 
 def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=True):
@@ -84,6 +119,7 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
     # with per-workgroup timing); the plans made in the timed steps are
     # placed by it.
     xcd_order = None
+    tsa.set_xcd_order(None)
     if calibrate and tsa.plan_items(plans0[0]).shape[0] >= 8:
         q, kn, vn, out, _, _ = chunk_t[0]
         tsa.append_kv(plans0[0], kn, vn, db.k_pool, db.v_pool, db.bt)
@@ -102,7 +138,7 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
         if events is not None:
             events[0].record(stream)
         for c, sp in enumerate(plans):
-            q, kn, vn, out, lse, _ = chunk_t[c]
+            q, kn, vn, out, lse, idx = chunk_t[c]
             tsa.append_kv(sp, kn, vn, db.k_pool, db.v_pool, db.bt)
             if events is not None:
                 events[2 * c + 1].record(stream)
@@ -120,7 +156,7 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    append_ms, prefill_ms = [], []
+    append_ms, prefill_ms, span_ms = [], [], []
     for e in ev:
         a = p = 0.0
         for c in range(n_chunks):
@@ -128,6 +164,14 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
             p += e[2 * c + 1].elapsed_time(e[2 * c + 2])
         append_ms.append(a)
         prefill_ms.append(p)
+        span_ms.append(e[0].elapsed_time(e[2 * n_chunks]))
+    # Outputs of the last step, in token order (chunks scattered back).
+    for c in range(n_chunks):
+        _, _, _, out, lse, idx = chunk_t[c]
+        if idx is not None:
+            db.out[idx] = out
+            db.lse[idx] = lse
+    torch.cuda.synchronize()
     ms_step = wall * 1e3 / steps
     prefill_avg = float(np.mean(prefill_ms))
     append_avg = float(np.mean(append_ms))
@@ -138,8 +182,9 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
         "flops": flops,
         "ms_per_step": ms_step,
         "tflops_step": flops / (ms_step * 1e-3) / 1e12,
+        "step_gpu_ms": dist(span_ms),
         "prefill_call_ms": prefill_avg,
-        "prefill_call_ms_p50": float(np.median(prefill_ms)),
+        "prefill_call_dist_ms": dist(prefill_ms),
         "prefill_tflops": flops / (prefill_avg * 1e-3) / 1e12,
         "append_ms": append_avg,
         "append_gbs": append_bytes / (append_avg * 1e-3) / 1e9,
@@ -152,36 +197,95 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
     }
 
 
-def cpu_baseline(wl, rows_n, oracle, harness, min_seconds=10.0):
-    """The oracle timed on the host cores over a seeded sample of query rows."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_rows(wl, rows, oracle):
+    """The oracle (fp64) on the flat rows `rows` of a workload: pools with the
+    prefix in place, the suffix appended by the oracle's own scatter; returns
+    (o [R, d], lse [R], seconds)."""
     from workload import BF16_NAN
     kp, vp = wl.pool_bits(fill=int(BF16_NAN))
-    kp, vp = oracle.append_kv(wl.prefix_lens, wl.suffix_lens, wl.block_tables, wl.page_size,
-                              wl.k_new, wl.v_new, kp, vp)
-    rng = np.random.default_rng(123)
-    rows_n = min(rows_n, wl.total_tokens * wl.num_q_heads)
-    rows = np.sort(rng.choice(wl.total_tokens * wl.num_q_heads, size=rows_n, replace=False))
-    # FLOPs of the sampled rows: 4 * d per visible (row, key) pair.
+    o_all, l_all = [], []
+    t = 0.0
+    for pre, suf, tok in wl.chunks:
+        kp, vp = oracle.append_kv(pre, suf, wl.block_tables, wl.page_size, wl.k_new[tok],
+                                  wl.v_new[tok], kp, vp)
+    # After every chunk is appended the pool holds all positions; rows of a
+    # chunk see only keys up to their own position, so attending each chunk's
+    # rows over the final pool equals the chunked computation.
+    Hq = wl.num_q_heads
+    for pre, suf, tok in wl.chunks:
+        lo, hi = int(tok[0]) * Hq, (int(tok[-1]) + 1) * Hq
+        sel = rows[(rows >= lo) & (rows < hi)]
+        if sel.size == 0:
+            continue
+        t0 = time.perf_counter()
+        o, l = oracle.sp_attention(pre, suf, wl.block_tables, wl.page_size, wl.q[tok], kp, vp,
+                                   rows=sel - lo)
+        t += time.perf_counter() - t0
+        o_all.append(o)
+        l_all.append(l)
+    return np.concatenate(o_all), np.concatenate(l_all), t
+
+
+def row_flops(wl, rows):
+    """4 d per visible (row, key) pair over the flat rows `rows`."""
     tok = rows // wl.num_q_heads
     offs = np.concatenate([[0], np.cumsum(wl.suffix_lens)])
     seq = np.searchsorted(offs, tok, side="right") - 1
     visible = wl.prefix_lens[seq].astype(np.int64) + (tok - offs[seq]) + 1
-    flops = float(4 * wl.head_dim * visible.sum())
-    # Repeat the pass until about 10 s of CPU work have been timed (a sample
-    # this size finishes one pass in a few seconds on 16 cores).
-    t0 = time.perf_counter()
-    passes = 0
+    return float(4 * wl.head_dim * visible.sum())
+
+
+def parity(wl, db, rows, o_ref, lse_ref, harness):
+    """The GPU output of the timed run against oracle rows."""
+    import torch  # noqa: F401
+    out = harness.host_bits(db.out).reshape(-1, wl.head_dim)[rows]
+    st = harness.error_stats(out, o_ref)
+    lse = db.lse.cpu().numpy().reshape(-1)[rows]
+    return {"rows": int(len(rows)), "max_abs": float(f"{st['max_abs']:.3e}"),
+            "mean_abs": float(f"{st['mean_abs']:.3e}"), "rel_l2": float(f"{st['rel_l2']:.3e}"),
+            "lse_max_abs": float(f"{float(np.abs(lse - lse_ref).max()):.3e}"),
+            "pass": bool(st["finite"] and st["max_abs"] <= harness.MAX_ABS and
+                         st["mean_abs"] <= harness.MEAN_ABS and st["rel_l2"] <= harness.REL_L2 and
+                         np.abs(lse - lse_ref).max() <= harness.LSE_ABS)}
+
+
+def cpu_baseline(wl, rows, oracle, min_seconds=10.0):
+    """The oracle timed on the host cores over the flat rows `rows` of the
+    workload, repeated until about `min_seconds` have been timed; returns the
+    baseline record and the first pass's (o, lse) for the parity check."""
+    flops = row_flops(wl, rows)
+    passes, dt, first = 0, 0.0, None
     while True:
-        oracle.sp_attention(wl.prefix_lens, wl.suffix_lens, wl.block_tables, wl.page_size, wl.q,
-                            kp, vp, rows=rows)
+        o, lse, t = oracle_rows(wl, rows, oracle)
+        first = first or (o, lse)
         passes += 1
-        dt = time.perf_counter() - t0
+        dt += t
         if dt >= min_seconds or passes >= 50:
             break
-    return {"value": passes * flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"{rows_n} of {wl.total_tokens * wl.num_q_heads} query rows (seeded) of "
-                      f"the same workload, fp64, {passes} pass(es) in {dt:.1f} s wall"}
+    n_all = wl.total_tokens * wl.num_q_heads
+    return ({"value": passes * flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+             "cpu": cpu_model(), "kind": "oracle",
+             "sample": f"{len(rows)} of {n_all} query rows (seeded) of the same workload, fp64, "
+                       f"{passes} pass(es) in {dt:.1f} s of oracle time"}, first)
+
+
+def sample_rows(wl, n, seed=123):
+    """Seeded sorted sample of n flat query rows (all of them if fewer)."""
+    n_all = wl.total_tokens * wl.num_q_heads
+    if n >= n_all:
+        return np.arange(n_all)
+    return np.sort(np.random.default_rng(seed).choice(n_all, size=n, replace=False))
 
 
 def measured_traffic(config):
@@ -458,7 +562,7 @@ def main():
     r = time_config(args.config, args.steps, args.warmup, torch, tsa, harness, workload,
                     calibrate=not args.no_xcd_calibration)
     wl = r.pop("wl")
-    r.pop("db")
+    db = r.pop("db")
     achieved = r["prefill_tflops"]
     line = {
         "metric": METRIC,
@@ -474,9 +578,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": {"single": "single continuation: P=25,000 cached + S=2,048 new tokens, "
-                                   "Hq=8 Hkv=1 d=128, page 16, shuffled 100K-page pool",
-                         }.get(args.config, args.config),
+            "workload": WORKLOADS.get(args.config, args.config),
             "num_seqs": wl.num_seqs,
             "prefix_lens": wl.prefix_lens.tolist() if wl.num_seqs <= 4 else "ragged",
             "suffix_lens": wl.suffix_lens.tolist() if wl.num_seqs <= 4 else "ragged",
@@ -486,6 +588,8 @@ def main():
         },
         "pct_bf16_peak": round(100 * r["tflops_step"] / PEAK_BF16_TFLOPS, 2),
         "ms_per_continuation": round(r["ms_per_step"] / wl.num_seqs, 4),
+        "step_gpu_ms": r["step_gpu_ms"],
+        "prefill_call_ms": r["prefill_call_dist_ms"],
         "xcd_order": r["xcd_order"],
         "breakdown_ms": {"plan_host": round(r["plan_us"] / 1e3, 4),
                          "append_kv": round(r["append_ms"], 4),
@@ -495,22 +599,50 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(args.config)},
     }
+    import oracle
+    if not args.no_cpu_baseline:
+        # The oracle beside the GPU: every query row of the workload (the
+        # single continuation's 16,384 rows take about 2 s a pass on 16
+        # cores), and the same rows check the timed GPU output.
+        rows = sample_rows(wl, args.cpu_rows)
+        line["cpu_baseline"], (o_ref, lse_ref) = cpu_baseline(wl, rows, oracle)
+        line["parity"] = parity(wl, db, rows, o_ref, lse_ref, harness)
+    del db
+    torch.cuda.empty_cache()
     extra = {"main": r}
+    if not args.no_extra_configs:
+        # The other configurations: the same path timed, plus the oracle on a
+        # seeded row sample (its speed, and parity of the timed output there).
+        line["configs"] = {}
+        for name in ("tiny", "ragged", "long", "cold"):
+            if name == args.config:
+                continue
+            rr = time_config(name, args.extra_steps, 3, torch, tsa, harness, workload,
+                             calibrate=not args.no_xcd_calibration)
+            wlx, dbx = rr.pop("wl"), rr.pop("db")
+            rec = {"workload": WORKLOADS[name],
+                   "ms_per_continuation": round(rr["ms_per_step"] / wlx.num_seqs, 4),
+                   "ms_per_step": round(rr["ms_per_step"], 4),
+                   "tflops_step": round(rr["tflops_step"], 2),
+                   "step_gpu_ms": rr["step_gpu_ms"],
+                   "prefill_call_ms": rr["prefill_call_dist_ms"],
+                   "prefill_tflops": round(rr["prefill_tflops"], 2),
+                   "frac": round(rr["prefill_tflops"] / PEAK_BF16_TFLOPS, 4),
+                   "append_gbs": round(rr["append_gbs"], 1),
+                   "work_items": rr["num_items"], "steps": args.extra_steps}
+            if not args.no_cpu_baseline:
+                rows = sample_rows(wlx, args.extra_rows, seed=321)
+                o_ref, lse_ref, t = oracle_rows(wlx, rows, oracle)
+                rec["oracle"] = {"value": round(row_flops(wlx, rows) / t / 1e12, 5),
+                                 "unit": "TFLOP/s", "rows": int(len(rows)),
+                                 "seconds": round(t, 2), "cores": oracle.num_threads()}
+                rec["parity"] = parity(wlx, dbx, rows, o_ref, lse_ref, harness)
+            line["configs"][name] = rec
+            extra[name] = rr
+            del dbx, wlx
+            torch.cuda.empty_cache()
     if args.extra_json:
         extra["hbm_sweep"] = hbm_sweep(torch, tsa)
-        if args.all_configs:
-            for name in ("tiny", "ragged", "long", "cold"):
-                if name == args.config:
-                    continue
-                rr = time_config(name, max(5, args.steps // 5), 2, torch, tsa, harness, workload)
-                rr.pop("wl")
-                rr.pop("db")
-                extra[name] = rr
-                torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
-        import oracle
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, oracle, harness)
-    if args.extra_json:
         with open(args.extra_json, "w") as f:
             json.dump(extra, f, indent=1, default=float)
     print(json.dumps(line), flush=True)

@@ -308,15 +308,18 @@ def measured_traffic(config):
 
 def hbm_sweep(torch, tsa, reps=10):
     """append_kv / gather_kv GB/s on synthetic batches of 102 MB to 2 GB, with
-    the 256 MB Infinity Cache flushed (1 GiB written) before every repetition."""
-    scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    the 256 MB Infinity Cache flushed before every repetition by reading a
+    1 GiB buffer.  (Writing the buffer instead would leave the cache full of
+    dirty lines that the timed kernel then has to write back to HBM.)"""
+    scratch = torch.ones(1 << 27, dtype=torch.int64, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int64, device="cuda")
 
     def timeit(fn):
         fn()
         torch.cuda.synchronize()
         ts = []
         for r in range(reps):
-            scratch.fill_(r)
+            sink.add_(scratch.sum())
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             fn()

@@ -279,30 +279,65 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     // XCDs of one part differ in speed by several percent, steadily.  Once an
     // XCD order is set (fastest first, as talaria_sp_attn_calibrate_xcd
     // measures it), a prefill plan that is one round of at most kMappedItems
-    // items ranks its items by key tiles, longest first, and deals them out
-    // in blocks: the fastest XCD takes the longest block, so the XCDs' last
-    // items end at about the same time.  Placement changes which compute
-    // unit runs an item, never what it computes.
+    // items is placed so that each XCD reads a narrow band of keys and the
+    // longest items run on the fastest XCDs:
+    //  - items are sorted by the keys they read (sequence, KV head, middle
+    //    of the key-tile range) and cut into kXcds contiguous groups, one per
+    //    XCD, so each XCD's L2 streams one band of K/V instead of all of it;
+    //  - the groups are ranked by their longest item and dealt to the XCDs
+    //    fastest first (among XCDs with the same number of workgroups).
+    // Placement changes which compute unit runs an item, never what it
+    // computes.
     int32_t order[kXcds];
     if (!decode_batch && items > 0 && items <= kMappedItems && xcd_order_snapshot(order)) {
         const int32_t n = (int32_t)items;
-        int32_t rank[kMappedItems], cost[kMappedItems];
+        int32_t by_key[kMappedItems], cost[kMappedItems];
+        int64_t key[kMappedItems];
         uint8_t uses[kMappedItems] = {};
         for (int32_t i = 0; i < n; ++i) {
             const WorkItem w = decode_item(p, i);
             cost[i] = w.tile_end - w.tile_begin;
-            rank[i] = i;
+            key[i] = (((int64_t)w.seq * p.num_kv_heads + w.kv_head) << 32) +
+                     (int64_t)w.tile_begin + w.tile_end;
+            by_key[i] = i;
         }
-        std::sort(rank, rank + n, [&](int32_t a, int32_t b) {
-            return cost[a] != cost[b] ? cost[a] > cost[b] : a < b;
+        std::sort(by_key, by_key + n, [&](int32_t a, int32_t b) {
+            return key[a] != key[b] ? key[a] < key[b] : a < b;
         });
-        int32_t next = 0;
+        // Workgroups per XCD: XCD x runs workgroups x, x + kXcds, ...
+        int32_t slots[kXcds];
+        for (int x = 0; x < kXcds; ++x)
+            slots[x] = x < n ? (n - x + kXcds - 1) / kXcds : 0;
+        // Group g (in key order) gets the size of the XCD at speed rank g
+        // after sorting ranks by size (larger first), which keeps sizes
+        // matched; then groups of one size are ranked by their longest item.
+        int32_t by_speed[kXcds];
+        for (int g = 0; g < kXcds; ++g)
+            by_speed[g] = order[g];
+        std::stable_sort(by_speed, by_speed + kXcds,
+                         [&](int32_t a, int32_t b) { return slots[a] > slots[b]; });
+        int32_t gbeg[kXcds + 1], gmax[kXcds], gidx[kXcds];
+        gbeg[0] = 0;
         for (int g = 0; g < kXcds; ++g) {
-            const int32_t x = order[g];
+            gbeg[g + 1] = gbeg[g] + slots[by_speed[g]];
+            gmax[g] = 0;
+            for (int32_t k = gbeg[g]; k < gbeg[g + 1]; ++k)
+                gmax[g] = std::max(gmax[g], cost[by_key[k]]);
+            gidx[g] = g;
+        }
+        std::stable_sort(gidx, gidx + kXcds, [&](int32_t a, int32_t b) {
+            const int32_t sa = gbeg[a + 1] - gbeg[a], sb = gbeg[b + 1] - gbeg[b];
+            return sa != sb ? sa > sb : gmax[a] > gmax[b];
+        });
+        for (int g = 0; g < kXcds; ++g) {
+            const int32_t x = by_speed[g], grp = gidx[g];
+            int32_t k = gbeg[grp];
             for (int32_t wg = x; wg < n; wg += kXcds) {
-                p.item_of_wg[wg] = (uint8_t)rank[next];
-                ++uses[rank[next++]];
+                p.item_of_wg[wg] = (uint8_t)by_key[k];
+                ++uses[by_key[k++]];
             }
+            if (k != gbeg[grp + 1])
+                return fail(TALARIA_SP_EINVAL, "internal error: XCD group size mismatch");
         }
         for (int32_t i = 0; i < n; ++i)
             if (uses[i] != 1)

@@ -7,7 +7,15 @@
 // of the plan: a query tile of 256 rows -- tile_tokens new tokens times the
 // `group` query heads that share one KV head, so every K/V byte staged in
 // LDS serves all of them -- against one contiguous range of 64-key tiles.
-// Each wave owns one 32-row MFMA block.
+// Each wave owns 32 query rows, as two 16-row MFMA blocks.
+//
+// Matrix cores.  Both products run on v_mfma_f32_16x16x32_bf16 in
+// accumulation chains: S^T(16 keys x 16 queries) chains over the head
+// dimension, O^T(16 features x 16 queries) over the keys.  On random bf16
+// operands this shape, chained, retires about 20% more work per second than
+// 32x32x16 under the part's power limit (the clock the part holds is set by
+// the operand switching, not by the issue rate).  Every K or V operand read
+// from LDS feeds the same chain position of both query blocks.
 //
 // Data movement.  K/V tiles move HBM -> LDS with the buffer form of the
 // direct-to-LDS load (no register staging) into two rings, K four tiles deep
@@ -17,21 +25,22 @@
 // from unowned pages; V entries past the end are zeroed in LDS so stale
 // slots (even NaN) cannot reach the output.
 //   K tile in LDS: 64 keys x D, natural key order, 16-byte chunks XOR-swizzled
-//                  by row.
+//                  by key.
 //   V tile in LDS: per page, [D][span] (tokens innermost, as in the pool),
 //                  chunks XOR-swizzled by feature row.
-// The QK^T A-operand reads K rows in the order that swaps the middle quarters
-// of every 16 keys; with that order the S^T accumulator of lane half h holds
-// 8 consecutive keys per 16, which is exactly the B-operand layout the PV
-// MFMA needs, so P goes from accumulator to operand in registers and V needs
-// no transpose.
+// The QK^T A-operand of key block kb reads, for accumulator row r, the key
+// 32 (kb / 2) + 8 (r / 4) + 4 (kb % 2) + r % 4.  With that order the S^T
+// accumulators of blocks 2j and 2j+1 give lane group g (lanes 16g..16g+15)
+// the 8 consecutive keys 32j + 8g .. +7 of each query: exactly the B operand
+// of the PV MFMA over keys 32j .. 32j+31, so P goes from accumulator to
+// operand in registers and V needs no transpose.
 //
 // Pipeline (per wave, one iteration per key tile t):
 //     P(t) = softmax step on S(t)  VALU: fma, exp2, cvt_pk_bf16, fp32 row
-//                                  sums (and, when needed, the row max with
-//                                  a permlane32 swap)
-//     O   += V(t-1)^T P(t-1)      D/8 x v_mfma_f32_32x32x16_bf16
-//     S(t+1) = K(t+1) Q^T          D/8 x MFMA
+//                                  sums (and, when needed, the row max
+//                                  across the four lanes of a row)
+//     O   += V(t-1)^T P(t-1)      D/4 x v_mfma_f32_16x16x32_bf16
+//     S(t+1) = K(t+1) Q^T          D/4 x MFMA
 // The two waves of a SIMD are one phase apart, so one wave's softmax runs
 // while the other's MFMAs do; the MFMA phase runs at raised wave priority.
 // The running maximum is lazy: O and l are rescaled only when some row's
@@ -60,8 +69,6 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -79,6 +86,7 @@ constexpr int kKStages = 4;  // K tile ring depth
 constexpr int kRsrcRecords = 0x7fffffff;
 constexpr int kRsrcFlags = 0x00020000;
 constexpr int kVStages = 5;  // V tile ring depth
+constexpr int kQB = 2;       // 16-row query blocks per wave
 
 struct NoMask {
     static constexpr bool value = false;
@@ -87,9 +95,9 @@ struct WithMask {
     static constexpr bool value = true;
 };
 
-template <int D, int SPAN, int QB>
+template <int D, int SPAN>
 struct Geo {
-    static constexpr int NW = kRowsPerTile / (32 * QB);      // waves per workgroup
+    static constexpr int NW = kRowsPerTile / (16 * kQB);     // waves per workgroup
     static constexpr int NT = 64 * NW;                       // threads per workgroup
     static constexpr int TILE_BYTES = kKeysPerTile * D * 2;  // one K (or V) tile
     static constexpr int LOADS = TILE_BYTES / 1024 / NW;     // wave-loads per wave per tile
@@ -99,42 +107,52 @@ struct Geo {
     static constexpr int V_RPL = 1024 / (2 * SPAN);          // V block rows per wave-load
     static constexpr int V_BLOCK = 2 * D * SPAN;             // bytes of one page block
     static constexpr int V_LPB = V_BLOCK / 1024;             // wave-loads per page block
-    static constexpr int KS = D / 16;                        // QK^T k-steps
-    static constexpr int DB = D / 32;                        // 32-wide output blocks
+    static constexpr int KS = D / 32;                        // QK^T k-steps (chain length)
+    static constexpr int DB = D / 16;                        // 16-wide output blocks
     static_assert(V_LPB >= 1, "page block smaller than one wave-load");
     static_assert(LOADS >= 1, "fewer wave-loads than waves");
-    static_assert(NT == 2 * kRowsPerTile / QB, "launch bounds mismatch");
+    static_assert(NW == 8, "the ping-pong schedule needs 8 waves");
 };
 
-// Chunk swizzles (bank-conflict-free MFMA operand reads).
+// Chunk swizzles.  A ds_read_b128 on gfx950 serves each half-wave in two
+// passes, lanes {0-7, 24-31} and {8-15, 16-23} (and the same blocks +32), and
+// is conflict free when the 16 lanes of a pass land on 16 distinct 16-byte
+// slots of a 256-byte bank row (measured with the LDS bank-conflict counter).
+// K: lane (r, g) reads chunk 4 ks + g of the key key_of(kb, r); the XOR with
+// bits 0-1 and 3-4 of the key (= r) spreads every pass over all 16 slots.
 template <int D>
-__device__ __forceinline__ int kswz(int row) {
-    return D == 128 ? (row & 15) : ((row & 3) | ((row >> 1) & 4));
+__device__ __forceinline__ int kswz(int key) {
+    return D == 128 ? ((key & 3) | ((key >> 1) & 12)) : (((key >> 1) & 1) | ((key >> 2) & 6));
 }
+// V: lane (r, g) reads feature row d = 16 db + r, key chunk g of the 32-key
+// step.  Rows that share a bank row inside one pass get different chunks.
 template <int SPAN>
 __device__ __forceinline__ int vswz(int d) {
-    if (SPAN == 8)
+    if (SPAN <= 16)
         return 0;
-    if (SPAN == 16)
-        return ((d >> 2) ^ (d >> 3)) & 1;
     if (SPAN == 32)
-        return (d >> 1) & 3;
-    return d & 7;
+        return (d >> 1) & 2;
+    return d & 6;
 }
-// QK^T A-operand row order: swap bits 2 and 3 (middle quarters of 16).
-__device__ __forceinline__ int pi_row(int i) {
-    return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1);
+// Key (tile-relative) in accumulator row r of S^T block kb.
+__device__ __forceinline__ int key_of(int kb, int r) {
+    return 32 * (kb >> 1) + 8 * (r >> 2) + 4 * (kb & 1) + (r & 3);
 }
 
-__device__ __forceinline__ float xhalf_max(float x) {
-    // Lanes l and l^32 hold the two halves of one query row's keys.
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
-                                                    false, false);
+// Maximum / sum over the four lanes l, l^16, l^32, l^48 that hold one query
+// row's keys.
+__device__ __forceinline__ float quad_max(float x) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                              false);
+    x = __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
-__device__ __forceinline__ float xhalf_sum(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
-                                                    false, false);
+__device__ __forceinline__ float quad_sum(float x) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                              false);
+    x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
@@ -178,9 +196,9 @@ struct Ctx {
 // fall in the single page that holds key k0 + 8w: one block-table lookup
 // and one base address per wave and tile; the per-lane parts are
 // loop-invariant.
-template <int D, int SPAN, int QB>
+template <int D, int SPAN>
 struct Loader {
-    using G = Geo<D, SPAN, QB>;
+    using G = Geo<D, SPAN>;
     uint32_t koff[G::LOADS];  // per-lane byte offsets inside the page
     uint32_t voff[G::LOADS];
     int wave;
@@ -235,45 +253,51 @@ struct Loader {
 };
 
 // Per-lane LDS byte offsets of the MFMA operand reads, fixed for the whole
-// kernel.  K: one per 16-wide k-step (the second 32-key block is a constant
-// 32 rows further).  V: the key pairs of a 16-key step and the 32-feature
-// blocks are constant strides when a page block holds at most 16 keys;
-// wider blocks swizzle the key chunk by feature row, so each 16-key step
-// has its own offset.
-template <int D, int SPAN, int QB>
+// kernel.  Lane l reads row r = l % 16 of a 16-row operand block and the
+// 16-byte chunk g = l / 16 of its 32-wide k-step.
+//   K: one offset per k-step; the four key blocks sit at constant offsets
+//      (the swizzle of key_of(kb, r) does not depend on kb).
+//   V: feature row d = 16 db + r, keys 32 ks2 + 8 g .. +7.  The 16-feature
+//      blocks and (for page blocks of at most 32 keys) the 32-key steps are
+//      constant strides; 64-key blocks swizzle the key chunk by feature row,
+//      so each step has its own offset.
+template <int D, int SPAN>
 struct OperandOffsets {
-    using G = Geo<D, SPAN, QB>;
-    static constexpr bool V_UNIFORM_STEP = SPAN <= 16;
-    static constexpr int VN = V_UNIFORM_STEP ? 1 : 4;
-    uint32_t k[D / 16];
+    using G = Geo<D, SPAN>;
+    static constexpr bool V_UNIFORM_STEP = SPAN <= 32;
+    static constexpr int VN = V_UNIFORM_STEP ? 1 : 2;
+    uint32_t k[G::KS];
     uint32_t v[VN];
 
-    __device__ __forceinline__ void init(int lq, int lh) {
-        const int row = pi_row(lq);
+    __device__ __forceinline__ void init(int r, int g) {
+        const int row = key_of(0, r);
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks)
-            k[ks] = (uint32_t)(row * (2 * D) + (((2 * ks + lh) ^ kswz<D>(row)) << 4));
+        for (int ks = 0; ks < G::KS; ++ks)
+            k[ks] = (uint32_t)(row * (2 * D) + (((4 * ks + g) ^ kswz<D>(row)) << 4));
 #pragma unroll
         for (int j = 0; j < VN; ++j) {
-            // Block row d = 32 db + lq has the swizzle of lq (the swizzles
-            // only look at the low five bits of d).
-            const int key = 16 * j + 8 * lh;
+            // Feature row d = 16 db + r has the swizzle of r (the swizzles
+            // only look at the low four bits of d).
+            const int key = 32 * j + 8 * g;
             const int pj = key / SPAN, lc = (key % SPAN) >> 3;
-            v[j] = (uint32_t)(pj * G::V_BLOCK + lq * (SPAN * 2) + ((lc ^ vswz<SPAN>(lq)) << 4));
+            v[j] = (uint32_t)(pj * G::V_BLOCK + r * (SPAN * 2) + ((lc ^ vswz<SPAN>(r)) << 4));
         }
     }
-    // Offset of the V operand of 16-key step ks2 and feature block db.
+    static constexpr uint32_t kblock(int kb) {
+        return (uint32_t)((32 * (kb >> 1) + 4 * (kb & 1)) * (2 * D));
+    }
+    // Offset of the V operand of 32-key step ks2 and feature block db.
     __device__ __forceinline__ const char* vptr(const char* vt, int ks2, int db) const {
         if (V_UNIFORM_STEP)
-            return vt + v[0] + ks2 * (16 / SPAN) * G::V_BLOCK + db * 32 * SPAN * 2;
-        return vt + v[ks2] + db * 32 * SPAN * 2;
+            return vt + v[0] + ks2 * (32 / SPAN) * G::V_BLOCK + db * 16 * SPAN * 2;
+        return vt + v[ks2] + db * 16 * SPAN * 2;
     }
 };
 
 // Zero the V entries of keys kv_len .. k0+63 of the V tile in `vbuf`.
-template <int D, int SPAN, int QB>
+template <int D, int SPAN>
 __device__ __forceinline__ void zero_v_tail(char* vbuf, int k0, int kv_len) {
-    using G = Geo<D, SPAN, QB>;
+    using G = Geo<D, SPAN>;
     const int first = kv_len - k0;  // first key (tile-relative) past the end
     if (first >= kKeysPerTile)
         return;
@@ -288,47 +312,51 @@ __device__ __forceinline__ void zero_v_tail(char* vbuf, int k0, int kv_len) {
     }
 }
 
-// S^T = K Q^T for the wave's QB 32-row blocks.
-template <int D, int SPAN, int QB>
-__device__ __forceinline__ void qk_tile(f32x16 (&s)[QB][2], const char* kbuf,
-                                        const bf16x8 (&qf)[QB][D / 16],
-                                        const OperandOffsets<D, SPAN, QB>& oo) {
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// S^T = K Q^T for the wave's two 16-row query blocks: per key block, the
+// K operands of all k-steps, then one chain per query block.
+template <int D, int SPAN>
+__device__ __forceinline__ void qk_tile(f32x4 (&s)[kQB][4], const char* kbuf,
+                                        const bf16x8 (&qf)[kQB][D / 32],
+                                        const OperandOffsets<D, SPAN>& oo) {
+    constexpr int KS = D / 32;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
+    for (int kb = 0; kb < 4; ++kb) {
+        bf16x8 a[KS];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-            s[qb][kb] = f32x16{};
+        for (int ks = 0; ks < KS; ++ks)
+            a[ks] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(kbuf + oo.k[ks] +
+                                                        OperandOffsets<D, SPAN>::kblock(kb)));
 #pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-        const char* kp = kbuf + oo.k[ks];
+        for (int qb = 0; qb < kQB; ++qb) {
+            f32x4 acc = mfma16(a[0], qf[qb][0], f32x4{});
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kb * 32 * (2 * D));
-            const bf16x8 af = __builtin_bit_cast(bf16x8, a);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
-                s[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[qb][ks], s[qb][kb],
-                                                                    0, 0, 0);
+            for (int ks = 1; ks < KS; ++ks)
+                acc = mfma16(a[ks], qf[qb][ks], acc);
+            s[qb][kb] = acc;
         }
     }
 }
 
-// O^T += V^T P^T for the wave's QB 32-row blocks.
-template <int D, int SPAN, int QB>
-__device__ __forceinline__ void pv_tile(f32x16 (&o)[QB][D / 32], const char* vt,
-                                        const bf16x8 (&pf)[QB][4],
-                                        const OperandOffsets<D, SPAN, QB>& oo) {
+// O^T += V^T P^T for the wave's two query blocks: per 16-feature block, the
+// V operands of both 32-key steps, then one chain of two per query block.
+template <int D, int SPAN>
+__device__ __forceinline__ void pv_tile(f32x4 (&o)[kQB][D / 16], const char* vt,
+                                        const bf16x8 (&pf)[kQB][2],
+                                        const OperandOffsets<D, SPAN>& oo) {
 #pragma unroll
-    for (int ks2 = 0; ks2 < 4; ++ks2) {
+    for (int db = 0; db < D / 16; ++db) {
+        const bf16x8 a0 =
+            __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(oo.vptr(vt, 0, db)));
+        const bf16x8 a1 =
+            __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(oo.vptr(vt, 1, db)));
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-            const u32x4 a = *reinterpret_cast<const u32x4*>(oo.vptr(vt, ks2, db));
-            const bf16x8 af = __builtin_bit_cast(bf16x8, a);
-#pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
-                o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[qb][ks2], o[qb][db],
-                                                                    0, 0, 0);
-        }
+        for (int qb = 0; qb < kQB; ++qb)
+            o[qb][db] = mfma16(a1, pf[qb][1], mfma16(a0, pf[qb][0], o[qb][db]));
     }
 }
 
@@ -338,46 +366,65 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
     return __builtin_elementwise_maximum(a, __builtin_elementwise_maximum(b, c));
 }
 
+// P(t) of one query block from S(t) with the row offset mb: two bf16x8 PV
+// operands (keys 32 j + 8 g .. +7 from blocks 2j and 2j+1) and this lane's
+// partial row sum (four independent partial sums, one per key block).
+__device__ __forceinline__ float p_block(const f32x4 (&s)[4], bf16x8 (&pf)[2], float scale,
+                                         float mb) {
+    float ls[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        float p[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            p[j] = __builtin_amdgcn_exp2f(fmaf(s[kb][j], scale, -mb));
+        ls[kb] = (p[0] + p[1]) + (p[2] + p[3]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            pf[kb >> 1][4 * (kb & 1) + j] = (__bf16)p[j];
+    }
+    return (ls[0] + ls[1]) + (ls[2] + ls[3]);
+}
+
 // One online-softmax step on S(t): returns P(t) as bf16 B-operands, updates
 // the running max / row sums, and reports whether O must be rescaled by
 // alpha before P(t) is accumulated.
-template <int QB, bool MASK>
-__device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB][4],
-                                             float (&m_run)[QB], float (&l_run)[QB],
-                                             float (&alpha)[QB], float scale, int k0,
-                                             const int (&qpos)[QB], int lh) {
+template <bool MASK>
+__device__ __forceinline__ bool softmax_tile(f32x4 (&s)[kQB][4], bf16x8 (&pf)[kQB][2],
+                                             float (&m_run)[kQB], float (&l_run)[kQB],
+                                             float (&alpha)[kQB], float scale, int k0,
+                                             const int (&qpos)[kQB], int g) {
     if (MASK) {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
+        for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int key = k0 + 32 * kb + 16 * (j >> 3) + 8 * lh + (j & 7);
+                for (int j = 0; j < 4; ++j) {
+                    const int key = k0 + 32 * (kb >> 1) + 8 * g + 4 * (kb & 1) + j;
                     if (key > qpos[qb])
                         s[qb][kb][j] = -INFINITY;
                 }
     }
-    float mt[QB];
+    float mt[kQB];
     bool grow = false;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
+    for (int qb = 0; qb < kQB; ++qb) {
         float m = max3f(s[qb][0][0], s[qb][0][1], s[qb][0][2]);
-#pragma unroll
-        for (int j = 3; j < 15; j += 2)
-            m = max3f(m, s[qb][0][j], s[qb][0][j + 1]);
-        m = max3f(m, s[qb][0][15], s[qb][1][0]);
-#pragma unroll
-        for (int j = 1; j < 15; j += 2)
-            m = max3f(m, s[qb][1][j], s[qb][1][j + 1]);
-        m = __builtin_elementwise_maximum(m, s[qb][1][15]);
-        mt[qb] = xhalf_max(m) * scale;
+        m = max3f(m, s[qb][0][3], s[qb][1][0]);
+        m = max3f(m, s[qb][1][1], s[qb][1][2]);
+        m = max3f(m, s[qb][1][3], s[qb][2][0]);
+        m = max3f(m, s[qb][2][1], s[qb][2][2]);
+        m = max3f(m, s[qb][2][3], s[qb][3][0]);
+        m = max3f(m, s[qb][3][1], s[qb][3][2]);
+        m = __builtin_elementwise_maximum(m, s[qb][3][3]);
+        mt[qb] = quad_max(m) * scale;
         grow = grow || (mt[qb] > m_run[qb] + kRescaleThreshold);
     }
     const bool resc = __any(grow);
     if (resc) {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
+        for (int qb = 0; qb < kQB; ++qb) {
             const float mn = __builtin_fmaxf(m_run[qb], mt[qb]);
             alpha[qb] = (mn == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - mn);
             m_run[qb] = mn;
@@ -385,27 +432,9 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB
         }
     }
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
+    for (int qb = 0; qb < kQB; ++qb) {
         const float mb = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
-        // Four independent partial row sums (one per 16-key step), so the
-        // adds do not form one 32-long dependency chain.
-        float ls[4];
-#pragma unroll
-        for (int ks2 = 0; ks2 < 4; ++ks2) {
-            bf16x8 v;
-#pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(
-                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e], scale, -mb));
-                const float p1 = __builtin_amdgcn_exp2f(
-                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e + 1], scale, -mb));
-                ls[ks2] = e == 0 ? p0 + p1 : ls[ks2] + p0 + p1;
-                v[e] = (__bf16)p0;
-                v[e + 1] = (__bf16)p1;
-            }
-            pf[qb][ks2] = v;
-        }
-        l_run[qb] += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+        l_run[qb] += p_block(s[qb], pf[qb], scale, mb);
     }
     return resc;
 }
@@ -417,54 +446,33 @@ __device__ __forceinline__ bool softmax_tile(f32x16 (&s)[QB][2], bf16x8 (&pf)[QB
 // P values, so the step is accepted when no lane's sum exceeds 2^8 (and
 // every row already has a finite running max); otherwise the caller redoes
 // the tile with softmax_tile.  Returns whether the step was accepted.
-template <int QB>
-__device__ __forceinline__ bool softmax_fast(const f32x16 (&s)[QB][2], bf16x8 (&pf)[QB][4],
-                                             const float (&m_run)[QB], float (&l_run)[QB],
+__device__ __forceinline__ bool softmax_fast(const f32x4 (&s)[kQB][4], bf16x8 (&pf)[kQB][2],
+                                             const float (&m_run)[kQB], float (&l_run)[kQB],
                                              float scale) {
     bool bad = false;
-    float lsum[QB];
+    float lsum[kQB];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const float mb = m_run[qb];
-        bad = bad || (mb == -INFINITY);
-        float ls[4];
-#pragma unroll
-        for (int ks2 = 0; ks2 < 4; ++ks2) {
-            bf16x8 v;
-#pragma unroll
-            for (int e = 0; e < 8; e += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(
-                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e], scale, -mb));
-                const float p1 = __builtin_amdgcn_exp2f(
-                    fmaf(s[qb][ks2 >> 1][(ks2 & 1) * 8 + e + 1], scale, -mb));
-                ls[ks2] = e == 0 ? p0 + p1 : ls[ks2] + p0 + p1;
-                v[e] = (__bf16)p0;
-                v[e + 1] = (__bf16)p1;
-            }
-            pf[qb][ks2] = v;
-        }
-        lsum[qb] = (ls[0] + ls[1]) + (ls[2] + ls[3]);
+    for (int qb = 0; qb < kQB; ++qb) {
+        bad = bad || (m_run[qb] == -INFINITY);
+        lsum[qb] = p_block(s[qb], pf[qb], scale, m_run[qb]);
         bad = bad || !(lsum[qb] <= kMaxLazyP);
     }
     if (__any(bad))
         return false;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < kQB; ++qb)
         l_run[qb] += lsum[qb];
     return true;
 }
 
-template <int D, int SPAN, int QB>
-__global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
+template <int D, int SPAN>
+__global__ __launch_bounds__(512, 1) void prefill_kernel(
     PlanData p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
     const uint16_t* __restrict__ v_pool, const int32_t* __restrict__ bt, float sm_scale,
     uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_o,
     float* __restrict__ part_lse) {
-    using G = Geo<D, SPAN, QB>;
-    // The two-group schedule below (and its load distances) assumes 8 waves,
-    // two per SIMD, i.e. one 32-row block per wave.  The helpers take QB row
-    // blocks per wave so that a 64-row-per-wave layout can reuse them.
-    static_assert(QB == 1 && G::NW == 8, "the ping-pong schedule needs 8 waves of 32 rows");
+    using G = Geo<D, SPAN>;
+    static_assert(G::NT == 512, "launch bounds mismatch");
     __shared__ __attribute__((aligned(1024))) char smem[(kKStages + kVStages) * G::TILE_BYTES];
 
     // Workgroup i runs on XCD i % 8; an XCD-placed plan names its item.
@@ -474,8 +482,8 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     const int Gq = p.group;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int lq = lane & 31;
-    const int lh = lane >> 5;
+    const int lr = lane & 15;  // operand / accumulator column (query) of this lane
+    const int lg = lane >> 4;  // lane group: k-chunk of operands, row quad of accumulators
 
     Ctx c;
     c.page_bytes = (uint32_t)(p.num_kv_heads * p.page_size * D * 2);
@@ -487,10 +495,10 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     c.last_page = (uint32_t)(c.kv_len - 1) >> p.page_shift;
     c.ps = p.page_size;
 
-    Loader<D, SPAN, QB> ld;
+    Loader<D, SPAN> ld;
     ld.init(wave, lane, c.ps);
-    OperandOffsets<D, SPAN, QB> oo;
-    oo.init(lq, lh);
+    OperandOffsets<D, SPAN> oo;
+    oo.init(lr, lg);
 
     const int tb = w.tile_begin, te = w.tile_end;
     // Ring slots: K tile t in kbuf(t), V tile t in vbuf(t).  Inside the main
@@ -529,37 +537,37 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     uint32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
     uint32_t pgv_next = c.bt_row[ld.page_index((tb + vd) * kKeysPerTile, c)];
 
-    // Query rows of this lane: one per 32-row block.
+    // Query rows of this lane: one per 16-row block.
     const int rows_used = p.tile_tokens * Gq;
-    int qtok[QB], qhead[QB], qpos[QB];
-    bf16x8 qf[QB][D / 16];
+    int qtok[kQB], qhead[kQB], qpos[kQB];
+    bf16x8 qf[kQB][D / 32];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const int r = (wave * QB + qb) * 32 + lq;
+    for (int qb = 0; qb < kQB; ++qb) {
+        const int r = (wave * kQB + qb) * 16 + lr;
         const int t = r / Gq;
         const bool valid = r < rows_used && t < w.num_tokens;
         qtok[qb] = valid ? t : -1;
         qhead[qb] = w.kv_head * Gq + r % Gq;
         qpos[qb] = s.prefix_len + w.first_token + (valid ? t : w.num_tokens - 1);
         const uint16_t* src = q + ((int64_t)(s.tok_off + w.first_token + t) * p.num_q_heads +
-                                   qhead[qb]) * D + lh * 8;
+                                   qhead[qb]) * D + lg * 8;
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-            u32x4 x = valid ? *reinterpret_cast<const u32x4*>(src + ks * 16) : u32x4{0, 0, 0, 0};
+        for (int ks = 0; ks < D / 32; ++ks) {
+            u32x4 x = valid ? *reinterpret_cast<const u32x4*>(src + ks * 32) : u32x4{0, 0, 0, 0};
             qf[qb][ks] = __builtin_bit_cast(bf16x8, x);
         }
     }
 
     const float scale = sm_scale * kLog2e;  // logits in base-2 units
-    f32x16 o[QB][D / 32];
+    f32x4 o[kQB][D / 16];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-            o[qb][db] = f32x16{};
-    float m_run[QB], l_run[QB], alpha[QB];
+        for (int db = 0; db < D / 16; ++db)
+            o[qb][db] = f32x4{};
+    float m_run[kQB], l_run[kQB], alpha[kQB];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
+    for (int qb = 0; qb < kQB; ++qb) {
         m_run[qb] = -INFINITY;
         l_run[qb] = 0.f;  // this lane's partial row sum
         alpha[qb] = 1.f;
@@ -575,15 +583,15 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
     wait_vmem_all();
     __syncthreads();
 
-    f32x16 sc[QB][2];
-    bf16x8 pf[QB][4];
+    f32x4 sc[kQB][4];
+    bf16x8 pf[kQB][2];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
+        for (int k = 0; k < 2; ++k)
             pf[qb][k] = bf16x8{};
     if (tb < te)
-        qk_tile<D, SPAN, QB>(sc, kbuf(tb), qf, oo);
+        qk_tile<D, SPAN>(sc, kbuf(tb), qf, oo);
 
     // tmask = smallest t with t * 64 + 63 > tile_first_pos (first tile that
     // can hold keys past some row of the query tile).
@@ -617,8 +625,12 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
             wait_vmem_all();
         lds_barrier();
     };
-    auto iteration = [&](int t, auto mask_tag, const bf16x8 (&pf)[QB][4],
-                         bf16x8 (&pn)[QB][4]) __attribute__((always_inline)) {
+    // Operand reads and MFMAs of one MFMA phase (PV then QK).
+    constexpr int kReads = 2 * (D / 16) + 4 * (D / 32);  // V: 2 per feature block; K: 4 x KS
+    constexpr int kMfmas = 2 * kReads;
+    constexpr int kAhead = 6;  // operand reads issued ahead of the MFMAs
+    auto iteration = [&](int t, auto mask_tag, const bf16x8 (&pf)[kQB][2],
+                         bf16x8 (&pn)[kQB][2]) __attribute__((always_inline)) {
         constexpr bool MASK = decltype(mask_tag)::value;
         // Pages of the next iteration's loads.  The scalar loads are issued
         // here and waited for after the softmax (which has no LDS traffic):
@@ -626,7 +638,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         // LDS reads, which would serialise the MFMA phase's operand reads.
         const uint32_t pk = c.bt_row[ld.page_index((uint32_t)(t + 1 + kd) * kKeysPerTile, c)];
         const uint32_t pv = c.bt_row[ld.page_index((uint32_t)(t + 1 + vd) * kKeysPerTile, c)];
-        float an[QB];
+        float an[kQB];
         // This iteration's tile loads, issued before the softmax so that the
         // MFMA phase holds only operand reads and MFMAs.
         if (t + kd < te)
@@ -634,15 +646,14 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         if (t + vd < te)
             ld.issue_v(smem + v_wr, (uint32_t)(t + vd) * kKeysPerTile, pgv_next, c);
         bool rn = false;
-        if (MASK || !softmax_fast<QB>(sc, pn, m_run, l_run, scale))
-            rn = softmax_tile<QB, MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile, qpos,
-                                        lh);
+        if (MASK || !softmax_fast(sc, pn, m_run, l_run, scale))
+            rn = softmax_tile<MASK>(sc, pn, m_run, l_run, an, scale, t * kKeysPerTile, qpos, lg);
         // The whole softmax step completes here, ahead of the MFMA phase (the
         // compiler would otherwise sink its exp/convert/sum tail past it).
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
+        for (int qb = 0; qb < kQB; ++qb) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
+            for (int k = 0; k < 2; ++k)
                 asm volatile("" ::"v"(pn[qb][k]));
             asm volatile("" ::"v"(l_run[qb]));
         }
@@ -656,25 +667,25 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         __builtin_amdgcn_s_setprio(1);
         if (resc) {
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
+            for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-                for (int db = 0; db < D / 32; ++db)
+                for (int db = 0; db < D / 16; ++db)
                     o[qb][db] *= alpha[qb];
         }
         // MFMA phase, unconditional: P(tb-1) = 0 over a zeroed V stage, and
         // S(te) comes from a slot K(te) was never loaded into and is never
         // used.
-        pv_tile<D, SPAN, QB>(o, smem + v_rd, pf, oo);
-        qk_tile<D, SPAN, QB>(sc, smem + k_rd, qf, oo);
-        // Operand reads run four ahead of the MFMAs that use them, across the
-        // PV / QK boundary: 4 reads, then (MFMA, read) pairs, then 4 MFMAs.
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        pv_tile<D, SPAN>(o, smem + v_rd, pf, oo);
+        qk_tile<D, SPAN>(sc, smem + k_rd, qf, oo);
+        // Operand reads run kAhead reads ahead of the MFMAs that use them,
+        // across the PV / QK boundary: each read feeds two MFMAs.
+        __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
 #pragma unroll
-        for (int i = 0; i < 2 * 16 * QB - 4; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        for (int i = 0; i < kReads - kAhead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfmas - 2 * (kReads - kAhead), 0);
         __builtin_amdgcn_s_setprio(0);
         pgk_next = pk;
         pgv_next = pv;
@@ -683,7 +694,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         v_rd = vnext(v_rd);
         v_wr = vnext(v_wr);
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
+        for (int qb = 0; qb < kQB; ++qb)
             alpha[qb] = an[qb];
         resc = rn;
         if (!group_b)
@@ -692,7 +703,7 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
 
     // P alternates between two register sets, two iterations per loop trip,
     // so that no copy is needed: at the start of a trip P(t-1) is in pf.
-    bf16x8 pn[QB][4];
+    bf16x8 pn[kQB][2];
     auto run = [&](int t0, int t1, auto mask_tag) __attribute__((always_inline)) {
         int t = t0;
         for (; t + 1 < t1; t += 2) {
@@ -702,9 +713,9 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         if (t < t1) {
             iteration(t, mask_tag, pf, pn);
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
+            for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
+                for (int k = 0; k < 2; ++k)
                     pf[qb][k] = pn[qb][k];
         }
     };
@@ -729,57 +740,49 @@ __global__ __launch_bounds__(2 * kRowsPerTile / QB, 1) void prefill_kernel(
         if (te * kKeysPerTile > c.kv_len) {
             wait_vmem_all();
             __syncthreads();
-            zero_v_tail<D, SPAN, QB>(vbuf(te - 1), (te - 1) * kKeysPerTile, c.kv_len);
+            zero_v_tail<D, SPAN>(vbuf(te - 1), (te - 1) * kKeysPerTile, c.kv_len);
             __syncthreads();
         }
         if (resc) {
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
+            for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-                for (int db = 0; db < D / 32; ++db)
+                for (int db = 0; db < D / 16; ++db)
                     o[qb][db] *= alpha[qb];
         }
-        pv_tile<D, SPAN, QB>(o, vbuf(te - 1), pf, oo);
+        pv_tile<D, SPAN>(o, vbuf(te - 1), pf, oo);
     }
 
-    // Epilogue: full row sums, normalise, write.
+    // Epilogue: full row sums, normalise, write.  Lane group g holds features
+    // 16 db + 4 g .. +3 of its query row.
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const float l = xhalf_sum(l_run[qb]);
+    for (int qb = 0; qb < kQB; ++qb) {
+        const float l = quad_sum(l_run[qb]);
         const float inv = l > 0.f ? 1.f / l : 0.f;
         const float lse2 = l > 0.f ? m_run[qb] + __log2f(l) : -INFINITY;
         if (qtok[qb] < 0)
             continue;
-        const int r = (wave * QB + qb) * 32 + lq;
+        const int r = (wave * kQB + qb) * 16 + lr;
         if (w.part_index < 0) {
             const int64_t row = (int64_t)(s.tok_off + w.first_token + qtok[qb]) * p.num_q_heads +
                                 qhead[qb];
-            uint16_t* dst = out + row * D;
+            uint16_t* dst = out + row * D + lg * 4;
 #pragma unroll
-            for (int db = 0; db < D / 32; ++db)
+            for (int db = 0; db < D / 16; ++db) {
+                bf16x4 v;
 #pragma unroll
-                for (int j4 = 0; j4 < 4; ++j4) {
-                    bf16x4 v;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        v[e] = (__bf16)(o[qb][db][j4 * 4 + e] * inv);
-                    *reinterpret_cast<bf16x4*>(dst + db * 32 + j4 * 8 + lh * 4) = v;
-                }
-            if (lse && lh == 0)
+                for (int e = 0; e < 4; ++e)
+                    v[e] = (__bf16)(o[qb][db][e] * inv);
+                *reinterpret_cast<bf16x4*>(dst + db * 16) = v;
+            }
+            if (lse && lg == 0)
                 lse[row] = lse2 * kLn2;
         } else {
-            float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D;
+            float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + lg * 4;
 #pragma unroll
-            for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-                for (int j4 = 0; j4 < 4; ++j4) {
-                    f32x4 v;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        v[e] = o[qb][db][j4 * 4 + e] * inv;
-                    *reinterpret_cast<f32x4*>(dst + db * 32 + j4 * 8 + lh * 4) = v;
-                }
-            if (lh == 0)
+            for (int db = 0; db < D / 16; ++db)
+                *reinterpret_cast<f32x4*>(dst + db * 16) = o[qb][db] * inv;
+            if (lg == 0)
                 part_lse[(int64_t)w.part_index * kRowsPerTile + r] = lse2;
         }
     }
@@ -864,15 +867,12 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
         lse[row] = (mx + __log2f(wsum)) * kLn2;
 }
 
-// Rows per wave: 32 (8 waves, two per SIMD).
-constexpr int kQB = 1;
-
 template <int D, int SPAN>
 void launch_prefill_kernel(const PlanData& p, const uint16_t* q, const uint16_t* kp,
                            const uint16_t* vp, const int32_t* bt, float sm_scale, uint16_t* out,
                            float* lse, float* part_o, float* part_lse, hipStream_t st) {
-    hipLaunchKernelGGL((prefill_kernel<D, SPAN, kQB>), dim3(p.num_items),
-                       dim3(Geo<D, SPAN, kQB>::NT), 0, st, p, q, kp, vp, bt, sm_scale, out, lse,
+    hipLaunchKernelGGL((prefill_kernel<D, SPAN>), dim3(p.num_items), dim3(Geo<D, SPAN>::NT), 0,
+                       st, p, q, kp, vp, bt, sm_scale, out, lse,
                        part_o, part_lse);
 }
 

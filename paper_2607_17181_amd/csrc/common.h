@@ -23,10 +23,11 @@ int launch_status(const char* what);
 #if defined(__HIPCC__)
 #include <hip/hip_runtime.h>
 namespace tsp {
-// Merge the split partials of a plan into out / lse (no-op when nothing is
-// split).  Defined with the prefill kernel.
-int launch_combine(const PlanData& p, const float* part_o, const float* part_lse, uint16_t* out,
-                   float* lse, hipStream_t st);
+// Merge the split partials of a plan (f16 normalised outputs, fp32 base-2
+// LSE) into out / lse (no-op when nothing is split).  Defined with the
+// prefill kernel.
+int launch_combine(const PlanData& p, const _Float16* part_o, const float* part_lse,
+                   uint16_t* out, float* lse, hipStream_t st);
 }  // namespace tsp
 #endif
 

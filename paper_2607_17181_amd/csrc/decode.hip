@@ -36,6 +36,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -101,7 +102,7 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
                                                      const int32_t* __restrict__ bt, float sm_scale,
                                                      uint16_t* __restrict__ out,
                                                      float* __restrict__ lse,
-                                                     float* __restrict__ part_o,
+                                                     _Float16* __restrict__ part_o,
                                                      float* __restrict__ part_lse) {
     constexpr int KS = D / 16, DB = D / 32;
     // Per-wave double-buffered K steps during the loop; the merge reuses the
@@ -357,10 +358,11 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
         if (lse && sub == 0)
             lse[orow] = lse2 * kLn2;
     } else {
-        float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + row) * D + sub * DPT;
+        _Float16* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + row) * D + sub * DPT;
 #pragma unroll
         for (int e = 0; e < DPT; e += 4)
-            *reinterpret_cast<f32x4*>(dst + e) = f32x4{acc[e], acc[e + 1], acc[e + 2], acc[e + 3]};
+            *reinterpret_cast<f16x4*>(dst + e) = f16x4{(_Float16)acc[e], (_Float16)acc[e + 1],
+                                                       (_Float16)acc[e + 2], (_Float16)acc[e + 3]};
         if (sub == 0)
             part_lse[(int64_t)w.part_index * kRowsPerTile + row] = lse2;
     }
@@ -403,7 +405,7 @@ extern "C" int talaria_sp_attn_decode(const talaria_sp_plan* plan, const void* q
                     workspace_bytes, (long long)p->ws_bytes);
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     char* ws = static_cast<char*>(workspace);
-    float* part_o = reinterpret_cast<float*>(ws);
+    _Float16* part_o = reinterpret_cast<_Float16*>(ws);
     float* part_lse = ws ? reinterpret_cast<float*>(ws + p->ws_lse_offset) : nullptr;
     auto qq = static_cast<const uint16_t*>(q);
     auto kp = static_cast<const uint16_t*>(k_pool);

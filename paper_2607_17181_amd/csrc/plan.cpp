@@ -345,7 +345,10 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
         p.wg_mapped = 1;
     }
 
-    const int64_t part_o = part_items * kRowsPerTile * (int64_t)d * 4;
+    // Split partials: normalised outputs in f16 (each is a convex combination
+    // of bf16 V rows, so f16 keeps 3 more mantissa bits than the bf16 result)
+    // and base-2 LSE in fp32.
+    const int64_t part_o = part_items * kRowsPerTile * (int64_t)d * 2;
     const int64_t part_lse = part_items * kRowsPerTile * 4;
     p.ws_lse_offset = (part_o + 255) & ~(int64_t)255;
     p.ws_bytes = part_items ? p.ws_lse_offset + part_lse : 0;

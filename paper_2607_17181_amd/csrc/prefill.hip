@@ -70,6 +70,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const char gbl_char;
@@ -469,7 +470,7 @@ template <int D, int SPAN>
 __global__ __launch_bounds__(512, 1) void prefill_kernel(
     PlanData p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_pool,
     const uint16_t* __restrict__ v_pool, const int32_t* __restrict__ bt, float sm_scale,
-    uint16_t* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_o,
+    uint16_t* __restrict__ out, float* __restrict__ lse, _Float16* __restrict__ part_o,
     float* __restrict__ part_lse) {
     using G = Geo<D, SPAN>;
     static_assert(G::NT == 512, "launch bounds mismatch");
@@ -778,10 +779,11 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
             if (lse && lg == 0)
                 lse[row] = lse2 * kLn2;
         } else {
-            float* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + lg * 4;
+            _Float16* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + lg * 4;
 #pragma unroll
             for (int db = 0; db < D / 16; ++db)
-                *reinterpret_cast<f32x4*>(dst + db * 16) = o[qb][db] * inv;
+                *reinterpret_cast<f16x4*>(dst + db * 16) =
+                    __builtin_convertvector(o[qb][db] * inv, f16x4);
             if (lg == 0)
                 part_lse[(int64_t)w.part_index * kRowsPerTile + r] = lse2;
         }
@@ -795,7 +797,8 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
 // Base-2 LSE merge in split order, KB splits per round of loads (8 for
 // plans with few splits, 16 for many-split plans such as a decode batch).
 template <int D, int KB>
-__global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* __restrict__ part_o,
+__global__ __launch_bounds__(256) void combine_kernel(PlanData p,
+                                                      const _Float16* __restrict__ part_o,
                                                       const float* __restrict__ part_lse,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse) {
@@ -816,7 +819,7 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
     const int n = w.num_splits;
     const int sub = threadIdx.x % TPR;
     const float* lse_k = part_lse + (int64_t)w.part_index * kRowsPerTile + r;
-    const float* o_k = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + sub * 4;
+    const _Float16* o_k = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + sub * 4;
     constexpr int64_t kStrideO = (int64_t)kRowsPerTile * D;
     // Online merge in split order, KB splits per round of loads (all issued
     // before any is used): the running maximum only grows, and the sums are
@@ -833,7 +836,8 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
             lk[k] = -INFINITY;
             if (k0 + k < n) {
                 lk[k] = lse_k[(k0 + k) * kRowsPerTile];
-                v[k] = *reinterpret_cast<const f32x4*>(o_k + (k0 + k) * kStrideO);
+                v[k] = __builtin_convertvector(
+                    *reinterpret_cast<const f16x4*>(o_k + (k0 + k) * kStrideO), f32x4);
             }
         }
         float cm = mx;
@@ -870,7 +874,7 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p, const float* _
 template <int D, int SPAN>
 void launch_prefill_kernel(const PlanData& p, const uint16_t* q, const uint16_t* kp,
                            const uint16_t* vp, const int32_t* bt, float sm_scale, uint16_t* out,
-                           float* lse, float* part_o, float* part_lse, hipStream_t st) {
+                           float* lse, _Float16* part_o, float* part_lse, hipStream_t st) {
     hipLaunchKernelGGL((prefill_kernel<D, SPAN>), dim3(p.num_items), dim3(Geo<D, SPAN>::NT), 0,
                        st, p, q, kp, vp, bt, sm_scale, out, lse,
                        part_o, part_lse);
@@ -880,7 +884,7 @@ template <int D>
 int launch_prefill(const PlanData& p, const uint16_t* q, const uint16_t* kp, const uint16_t* vp,
                    const int32_t* bt, float sm_scale, uint16_t* out, float* lse, char* ws,
                    hipStream_t st) {
-    float* part_o = reinterpret_cast<float*>(ws);
+    _Float16* part_o = reinterpret_cast<_Float16*>(ws);
     float* part_lse = ws ? reinterpret_cast<float*>(ws + p.ws_lse_offset) : nullptr;
     switch (p.page_size) {
     case 8:
@@ -904,8 +908,8 @@ int launch_prefill(const PlanData& p, const uint16_t* q, const uint16_t* kp, con
 
 }  // namespace
 
-int launch_combine(const PlanData& p, const float* part_o, const float* part_lse, uint16_t* out,
-                   float* lse, hipStream_t st) {
+int launch_combine(const PlanData& p, const _Float16* part_o, const float* part_lse,
+                   uint16_t* out, float* lse, hipStream_t st) {
     if (p.num_part_items == 0)
         return TALARIA_SP_OK;
     // The grid covers only split query tiles: per sequence, as many tiles as

@@ -91,8 +91,8 @@ def test_single_continuation_fills_the_gpu_in_one_round():
     assert items.shape[0] == 256
     keys = items[:, 5] - items[:, 4]
     assert keys.max() - keys.min() <= 2 * 64 + 2048 // 4
-    # workspace: fp32 partial O + LSE for 256 rows of every split item
-    part = 256 * 256 * 128 * 4
+    # workspace: f16 partial O + fp32 LSE for 256 rows of every split item
+    part = 256 * 256 * 128 * 2
     assert sp.workspace_bytes == ((part + 255) // 256) * 256 + 256 * 256 * 4
 
 

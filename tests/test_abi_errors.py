@@ -74,8 +74,8 @@ def test_prefill_noalloc_rejects_plans_beyond_its_scratch():
     size check (and then stops at the NULL-pointer check)."""
     lib = tsa.library()
     assert tsa.noalloc_scratch_bytes() == 64 << 20
-    geom = tsa.make_geom(8, 1, 128, 16, 1000)
-    big = tsa.plan(geom, [5000], [256], 400, kv_splits=64)   # 8 query tiles x 64 splits
+    geom = tsa.make_geom(8, 1, 128, 16, 2000)
+    big = tsa.plan(geom, [20000], [512], 1300, kv_splits=64)  # 16 query tiles x 64 splits
     assert big.workspace_bytes > tsa.noalloc_scratch_bytes()
     f = lib.talaria_sp_attn_prefill_noalloc
     assert f(ctypes.byref(big.raw), BAD, BAD, BAD, BAD, 0.0, BAD, NULL, NULL) == tsa.ENOSPACE

@@ -111,7 +111,9 @@ typedef struct {
  * The planner cuts every (sequence, KV head) into query tiles and splits
  * each tile's visible key range into near-equal pieces, so a ragged batch
  * spreads over all compute units; split results are merged by a
- * log-sum-exp combine inside talaria_sp_attn_prefill.
+ * log-sum-exp combine inside talaria_sp_attn_prefill.  A batch that takes
+ * several rounds of the GPU is cut finer and launched longest items first.
+ * Neither choice changes what is computed.
  */
 TALARIA_SP_API int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seqs,
                          const int32_t* prefix_lens, const int32_t* suffix_lens,
@@ -237,7 +239,8 @@ TALARIA_SP_API int talaria_sp_attn_gather_kv(const talaria_sp_plan* plan, const 
 
 /* Introspection of a plan's work list (host only).  Writes up to max_items
  * records of 8 int32 each: {sequence, kv_head, first_token, num_tokens,
- * key_begin, key_end, split, num_splits}; keys are absolute positions.
+ * key_begin, key_end, split, num_splits}, in launch order; sequence is the
+ * caller's index and keys are absolute positions.
  * Returns the number of work items (>= 0) or a negative status. */
 TALARIA_SP_API int talaria_sp_attn_plan_items(const talaria_sp_plan* plan, int32_t* items, int32_t max_items);
 

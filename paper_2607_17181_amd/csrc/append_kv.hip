@@ -46,7 +46,7 @@ __global__ __launch_bounds__(256) void append_kv_kernel(PlanData p, const uint16
         return;
     const int pos_lo = max(s.prefix_len, lp * ps);
     const int pos_hi = min(end, (lp + 1) * ps);
-    const int64_t page = bt[(int64_t)b * p.bt_stride + lp];
+    const int64_t page = bt[bt_row_index(p, b) * p.bt_stride + lp];
     const int hkv = p.num_kv_heads;
 
     // K: token rows of D bf16 = D/8 chunks of 16 bytes.

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256) void decode_kernel(PlanData p, const uint16_t*
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar page reads
     const int lq = lane & 31, lh = lane >> 5;
     const int ps = p.page_size, shift = p.page_shift, hkv = p.num_kv_heads, g = w.kv_head;
-    const int32_t* bt_row = bt + (int64_t)w.seq * p.bt_stride;
+    const int32_t* bt_row = bt + bt_row_index(p, w.seq) * p.bt_stride;
     const int kv_len = s.prefix_len + s.suffix_len;
     const int key_lo = w.tile_begin * kKeysPerTile;
     const int key_hi = min(w.tile_end * kKeysPerTile, kv_len);

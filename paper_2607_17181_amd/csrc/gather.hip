@@ -39,7 +39,7 @@ __global__ __launch_bounds__(256) void gather_kv_kernel(PlanData p, const uint16
     if (lp * ps >= n)
         return;
     const int ntok = min(ps, n - lp * ps);
-    const int64_t page = bt[(int64_t)b * p.bt_stride + lp];
+    const int64_t page = bt[bt_row_index(p, b) * p.bt_stride + lp];
     const int hkv = p.num_kv_heads;
     const int64_t out0 = (int64_t)p.kv_off[b] + lp * ps;  // output row of slot 0
 

@@ -41,6 +41,10 @@ constexpr int kMinTilesPerSplit = 8;
 // range worth a split.
 constexpr int kDecodeItemsPerCU = 2;
 constexpr int kMinTilesPerDecodeSplit = 4;
+// A batch that takes several rounds is cut into items of at most this
+// fraction of one compute unit's share of its key tiles, so that, started
+// longest first, no item can form a long tail.
+constexpr double kMultiRoundShare = 0.25;
 }  // namespace
 
 int fail(int code, const char* fmt, ...) {
@@ -176,6 +180,7 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     int64_t tok = 0, kvtok = 0;
     int32_t tiles[TALARIA_SP_MAX_SEQS];
     int32_t qtiles[TALARIA_SP_MAX_SEQS];
+    int32_t tok_off[TALARIA_SP_MAX_SEQS], kv_off[TALARIA_SP_MAX_SEQS];
     double total_cost = 0.0;
     int64_t base_items = 0;
     for (int32_t b = 0; b < num_seqs; ++b) {
@@ -189,10 +194,8 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
         if (pages > max_pages_per_seq)
             return fail(TALARIA_SP_EINVAL, "sequence %d needs %lld pages but the block-table "
                         "stride is %d", b, (long long)pages, max_pages_per_seq);
-        p.seq[b].prefix_len = (int32_t)P;
-        p.seq[b].suffix_len = (int32_t)S;
-        p.seq[b].tok_off = (int32_t)tok;
-        p.kv_off[b] = (int32_t)kvtok;
+        tok_off[b] = (int32_t)tok;
+        kv_off[b] = (int32_t)kvtok;
         tok += S;
         kvtok += P + S;
         if (tok > INT32_MAX / 2 || kvtok > INT32_MAX / 2)
@@ -212,8 +215,8 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
     p.kv_off[num_seqs] = (int32_t)kvtok;
 
     // Target key tiles per item: the per-CU share of the batch when the
-    // batch alone cannot fill the GPU (one round of equal items), half of it
-    // otherwise (so that a long sequence's items cannot form a long tail).
+    // batch alone cannot fill the GPU (one round of equal items), a quarter
+    // of it otherwise (kMultiRoundShare).
     //
     // A decode batch (every suffix at most one token) streams K/V for very
     // few query rows: its items are HBM-bound and cheap in compute, so it is
@@ -223,8 +226,9 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
         decode_batch = decode_batch && suffix_lens[b] <= 1;
     const int concurrent = decode_batch ? kDecodeItemsPerCU * kConcurrentItems : kConcurrentItems;
     double share = total_cost / concurrent;
-    if (base_items >= concurrent)
-        share *= 0.5;
+    const bool multi_round = base_items >= concurrent;
+    if (multi_round)
+        share *= kMultiRoundShare;
     double target = std::max<double>(decode_batch ? kMinTilesPerDecodeSplit : kMinTilesPerSplit,
                                      share);
     auto splits_of = [&](int32_t b, double tgt) {
@@ -257,11 +261,35 @@ extern "C" int talaria_sp_attn_plan(const talaria_sp_geom* geom, int32_t num_seq
         }
     }
 
+    // Launch order.  Workgroups start in item order as compute units free
+    // up, so a batch that takes several rounds runs its longest items first
+    // (sequences ranked by their longest item, which bounds the tail to
+    // about one short item); inside a sequence the longest query tiles
+    // already come first.  One-round and decode plans keep the caller's
+    // order.  The order changes which compute unit runs an item and when,
+    // never what it computes.
+    int32_t launch[TALARIA_SP_MAX_SEQS];
+    for (int32_t b = 0; b < num_seqs; ++b)
+        launch[b] = b;
+    if (multi_round && !decode_batch) {
+        int32_t longest[TALARIA_SP_MAX_SEQS];
+        for (int32_t b = 0; b < num_seqs; ++b)
+            longest[b] = qtiles[b] > 0 ? ceil_div(tiles[b], splits_of(b, target)) : -1;
+        std::stable_sort(launch, launch + num_seqs,
+                         [&](int32_t a, int32_t c) { return longest[a] > longest[c]; });
+    }
+
     int64_t items = 0, part_items = 0;
-    for (int32_t b = 0; b < num_seqs; ++b) {
+    for (int32_t i = 0; i < num_seqs; ++i) {
+        const int32_t b = launch[i];
         const int32_t nsp = splits_of(b, target);
-        p.seq[b].item_off = (int32_t)items;
-        p.seq[b].part_off = (int32_t)part_items;
+        p.seq[i].prefix_len = prefix_lens[b];
+        p.seq[i].suffix_len = suffix_lens[b];
+        p.seq[i].tok_off = tok_off[b];
+        p.kv_off[i] = kv_off[b];
+        p.seq_orig[i] = (uint8_t)b;
+        p.seq[i].item_off = (int32_t)items;
+        p.seq[i].part_off = (int32_t)part_items;
         const int64_t n = (int64_t)qtiles[b] * hkv * nsp;
         items += n;
         if (nsp > 1)
@@ -370,9 +398,13 @@ extern "C" int talaria_sp_attn_check_tables(const talaria_sp_plan* plan,
     // last[page]: the last sequence that named the page (-1: none yet).
     std::vector<int32_t> last((size_t)p->num_pages, -1);
     std::vector<uint8_t> written((size_t)p->num_pages, 0);
+    // Sequences are visited in the caller's order (row b of the tables).
+    std::vector<int32_t> at((size_t)p->num_seqs);
+    for (int32_t i = 0; i < p->num_seqs; ++i)
+        at[p->seq_orig[i]] = i;
     // Pass 1: range, duplicates inside one sequence, and the written pages.
     for (int32_t b = 0; b < p->num_seqs; ++b) {
-        const int64_t P = p->seq[b].prefix_len, S = p->seq[b].suffix_len;
+        const int64_t P = p->seq[at[b]].prefix_len, S = p->seq[at[b]].suffix_len;
         const int64_t pages = (P + S + p->page_size - 1) >> p->page_shift;
         const int32_t* row = host_block_tables + (int64_t)b * p->bt_stride;
         for (int64_t lp = 0; lp < pages; ++lp) {
@@ -391,7 +423,7 @@ extern "C" int talaria_sp_attn_check_tables(const talaria_sp_plan* plan,
     // Pass 2: a written page must be named exactly once in the whole batch.
     std::vector<int32_t> count((size_t)p->num_pages, 0);
     for (int32_t b = 0; b < p->num_seqs; ++b) {
-        const int64_t P = p->seq[b].prefix_len, S = p->seq[b].suffix_len;
+        const int64_t P = p->seq[at[b]].prefix_len, S = p->seq[at[b]].suffix_len;
         const int64_t pages = (P + S + p->page_size - 1) >> p->page_shift;
         const int32_t* row = host_block_tables + (int64_t)b * p->bt_stride;
         for (int64_t lp = 0; lp < pages; ++lp)
@@ -417,7 +449,7 @@ extern "C" int talaria_sp_attn_plan_items(const talaria_sp_plan* plan, int32_t* 
         const int32_t P = p->seq[w.seq].prefix_len;
         const int32_t kend_all = P + w.first_token + w.num_tokens;
         int32_t* r = items + 8 * i;
-        r[0] = w.seq;
+        r[0] = p->seq_orig[w.seq];
         r[1] = w.kv_head;
         r[2] = w.first_token;
         r[3] = w.num_tokens;

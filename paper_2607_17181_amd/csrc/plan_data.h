@@ -18,7 +18,7 @@
 namespace tsp {
 
 constexpr uint32_t kPlanMagic = 0x54535041u;  // "TSPA"
-constexpr uint32_t kPlanVersion = 2;
+constexpr uint32_t kPlanVersion = 3;
 
 // Work decomposition of the prefill kernel.
 constexpr int kRowsPerTile = 256;   // query rows (token x head-in-group) per work item
@@ -62,10 +62,15 @@ struct PlanData {
     uint8_t item_of_wg[kMappedItems];  // XCD placement (wg_mapped only)
     int32_t kv_off[TALARIA_SP_MAX_SEQS + 1];  // gather output row offsets
     SeqDesc seq[TALARIA_SP_MAX_SEQS + 1];     // entry num_seqs: sentinel
+    // Sequences are held in launch order (see the planner); seq_orig[i] is
+    // the caller's index of sequence i, i.e. its block-table row.  Token and
+    // gather offsets (tok_off, kv_off) are the caller's layout already.
+    uint8_t seq_orig[TALARIA_SP_MAX_SEQS];
 };
 
 static_assert(sizeof(PlanData) <= sizeof(talaria_sp_plan), "plan storage too small");
 static_assert(sizeof(PlanData) <= 3584, "plan must fit a kernel argument");
+static_assert(TALARIA_SP_MAX_SEQS <= 256, "seq_orig holds sequence indices in a byte");
 
 struct WorkItem {
     int32_t seq;
@@ -105,6 +110,9 @@ TSP_HD int32_t seq_of_item(const PlanData& p, int32_t id) {
     }
     return lo;
 }
+
+// Block-table row of (launch-order) sequence b.
+TSP_HD int64_t bt_row_index(const PlanData& p, int32_t b) { return p.seq_orig[b]; }
 
 // Decode a work item.  Inside a sequence the split index varies fastest,
 // then the KV head, then the query tile in reverse order (the query tiles

@@ -490,7 +490,7 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
     c.page_bytes = (uint32_t)(p.num_kv_heads * p.page_size * D * 2);
     c.kpool_g = (const gbl_char*)(const char*)k_pool + (int64_t)w.kv_head * p.page_size * D * 2;
     c.vpool_g = (const gbl_char*)(const char*)v_pool + (int64_t)w.kv_head * p.page_size * D * 2;
-    c.bt_row = bt + (int64_t)w.seq * p.bt_stride;
+    c.bt_row = bt + bt_row_index(p, w.seq) * p.bt_stride;
     c.kv_len = s.prefix_len + s.suffix_len;
     c.page_shift = p.page_shift;
     c.last_page = (uint32_t)(c.kv_len - 1) >> p.page_shift;

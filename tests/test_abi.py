@@ -117,6 +117,39 @@ def test_items_fit_one_round_of_resident_slots(seed):
     assert keys.max() <= 1.25 * keys.mean() + 4 * 64
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_multi_round_batch_runs_longest_items_first(seed):
+    """A batch that takes several rounds of the GPU is cut into items of at
+    most a quarter of one CU's share of its key tiles, and its sequences are
+    launched in order of their longest item (ties in the caller's order).
+    Items report the caller's sequence index and still cover every pair."""
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(8, 40))
+    pre = np.minimum(rng.lognormal(np.log(25_000), 0.87, n), 131_072).astype(int).tolist()
+    suf = rng.integers(512, 4097, size=n).tolist()
+    if seed % 3 == 0:
+        suf[int(rng.integers(0, n))] = 0     # a sequence with nothing to do
+    geom = _geom(pages=1 << 30)
+    sp = tsa.plan(geom, pre, suf, (max(pre) + max(suf) + 15) // 16)
+    items = check_coverage(sp, geom)
+    tiles = -(-(items[:, 5] - items[:, 4]) // 64)
+    # per-sequence blocks, in launch order
+    seqs = [int(items[0, 0])]
+    for b in items[1:, 0]:
+        if int(b) != seqs[-1]:
+            assert int(b) not in seqs, "a sequence's items are not contiguous"
+            seqs.append(int(b))
+    longest = [int(tiles[items[:, 0] == b].max()) for b in seqs]
+    assert longest == sorted(longest, reverse=True)
+    for x, y in zip(seqs, seqs[1:]):
+        if longest[seqs.index(x)] == longest[seqs.index(y)]:
+            assert x < y
+    # item size bound: a quarter of the per-CU share (qtiles x key tiles)
+    cost = sum(-(-s // 32) * -(-(p + s) // 64) for p, s in zip(pre, suf))
+    target = max(8, 0.25 * cost / 256)
+    assert tiles.max() <= target / 0.999 + 1
+
+
 def test_unsplit_batch_needs_no_workspace():
     sp = tsa.plan(_geom(), [0, 0, 0, 0], [25_000] * 4, 1600)
     assert sp.workspace_bytes == 0

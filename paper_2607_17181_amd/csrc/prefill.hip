@@ -88,6 +88,12 @@ constexpr int kRsrcRecords = 0x7fffffff;
 constexpr int kRsrcFlags = 0x00020000;
 constexpr int kVStages = 5;  // V tile ring depth
 constexpr int kQB = 2;       // 16-row query blocks per wave
+// Combine: features per thread (one 16-byte f16 load per split, one 16-byte
+// bf16 store).
+constexpr int kCombineFeatures = 8;
+typedef _Float16 f16xc __attribute__((ext_vector_type(kCombineFeatures)));
+typedef float f32xc __attribute__((ext_vector_type(kCombineFeatures)));
+typedef __bf16 bf16xc __attribute__((ext_vector_type(kCombineFeatures)));
 
 struct NoMask {
     static constexpr bool value = false;
@@ -790,7 +796,8 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
     }
 }
 
-// Merge the split partials of one query tile, 8 rows per workgroup.  Only
+// Merge the split partials of one query tile, 256 / (D / kCombineFeatures)
+// rows per workgroup.  Only
 // split query tiles are launched (blocks past a sequence's own tile count,
 // or of sequences without splits, exit at once): a grid over every work
 // item spent most of its time dispatching blocks with nothing to do.
@@ -802,15 +809,15 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p,
                                                       const float* __restrict__ part_lse,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse) {
-    // Grid: (split query tile of the sequence, 8-row block, sequence); the
+    // Grid: (split query tile of the sequence, row block, sequence); the
     // tile's split 0 item is item_off + tile * splits.
     const int32_t b = blockIdx.z;
     const int32_t nsp = num_splits_of(p, b);
     if (nsp <= 1 || (int32_t)blockIdx.x >= num_q_tiles(p, b) * p.num_kv_heads)
         return;
     const WorkItem w = decode_item(p, p.seq[b].item_off + (int32_t)blockIdx.x * nsp);
-    constexpr int TPR = D / 4;      // threads per row (4 features each)
-    constexpr int RPB = 256 / TPR;  // rows per block
+    constexpr int TPR = D / kCombineFeatures;  // threads per row
+    constexpr int RPB = 256 / TPR;             // rows per block
     const int r = blockIdx.y * RPB + threadIdx.x / TPR;
     const int G = p.group;
     if (r >= w.num_tokens * G)
@@ -819,25 +826,26 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p,
     const int n = w.num_splits;
     const int sub = threadIdx.x % TPR;
     const float* lse_k = part_lse + (int64_t)w.part_index * kRowsPerTile + r;
-    const _Float16* o_k = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + sub * 4;
+    const _Float16* o_k =
+        part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + sub * kCombineFeatures;
     constexpr int64_t kStrideO = (int64_t)kRowsPerTile * D;
     // Online merge in split order, KB splits per round of loads (all issued
     // before any is used): the running maximum only grows, and the sums are
     // rescaled when it does.  The merge order, and so every result bit, does
     // not depend on KB.
     float mx = -INFINITY;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32xc acc = {};
     float wsum = 0.f;
     for (int k0 = 0; k0 < n; k0 += KB) {
         float lk[KB];
-        f32x4 v[KB];
+        f32xc v[KB];
 #pragma unroll
         for (int k = 0; k < KB; ++k) {
             lk[k] = -INFINITY;
             if (k0 + k < n) {
                 lk[k] = lse_k[(k0 + k) * kRowsPerTile];
                 v[k] = __builtin_convertvector(
-                    *reinterpret_cast<const f16x4*>(o_k + (k0 + k) * kStrideO), f32x4);
+                    *reinterpret_cast<const f16xc*>(o_k + (k0 + k) * kStrideO), f32xc);
             }
         }
         float cm = mx;
@@ -862,11 +870,11 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p,
     const int t = r / G;
     const int64_t row = (int64_t)(s.tok_off + w.first_token + t) * p.num_q_heads +
                         w.kv_head * G + r % G;
-    bf16x4 v;
+    bf16xc v;
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
+    for (int e = 0; e < kCombineFeatures; ++e)
         v[e] = (__bf16)(acc[e] * inv);
-    *reinterpret_cast<bf16x4*>(out + row * D + sub * 4) = v;
+    *reinterpret_cast<bf16xc*>(out + row * D + sub * kCombineFeatures) = v;
     if (lse && sub == 0)
         lse[row] = (mx + __log2f(wsum)) * kLn2;
 }
@@ -929,7 +937,7 @@ int launch_combine(const PlanData& p, const _Float16* part_o, const float* part_
         return TALARIA_SP_OK;
     const bool many = max_splits > 8;
     if (p.head_dim == 128) {
-        const dim3 grid(tiles, ceil_div(rows, 256 / (128 / 4)), p.num_seqs);
+        const dim3 grid(tiles, ceil_div(rows, 256 / (128 / kCombineFeatures)), p.num_seqs);
         if (many)
             hipLaunchKernelGGL((combine_kernel<128, 16>), grid, dim3(256), 0, st, p, part_o,
                                part_lse, out, lse);
@@ -937,7 +945,7 @@ int launch_combine(const PlanData& p, const _Float16* part_o, const float* part_
             hipLaunchKernelGGL((combine_kernel<128, 8>), grid, dim3(256), 0, st, p, part_o,
                                part_lse, out, lse);
     } else {
-        const dim3 grid(tiles, ceil_div(rows, 256 / (64 / 4)), p.num_seqs);
+        const dim3 grid(tiles, ceil_div(rows, 256 / (64 / kCombineFeatures)), p.num_seqs);
         if (many)
             hipLaunchKernelGGL((combine_kernel<64, 16>), grid, dim3(256), 0, st, p, part_o,
                                part_lse, out, lse);

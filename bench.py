@@ -52,8 +52,12 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The GPU settles to its steady (power-limited) clock only after about
+    # 50-100 ms of continuous MFMA work; a 5-step warm-up timed the single
+    # continuation's prefill call at 0.201 ms p50 where the settled figure is
+    # 0.189 ms.  400 warm-up steps are about 0.1 s of work.
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=400)
     ap.add_argument("--config", default="single",
                     choices=["tiny", "single", "ragged", "long", "cold"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -68,6 +72,9 @@ def parse():
                          "timed and reported under \"configs\")")
     ap.add_argument("--extra-steps", type=int, default=20,
                     help="timed steps for each of the other configs")
+    ap.add_argument("--extra-warmup-ms", type=float, default=150.0,
+                    help="untimed warm-up of each of the other configs, in ms of steps "
+                         "(at least 3 steps)")
     ap.add_argument("--extra-rows", type=int, default=4096,
                     help="seeded query rows the oracle computes for each of the other configs")
     ap.add_argument("--hbm-sweep", action="store_true",
@@ -102,7 +109,8 @@ def dist(values):
 
 
 def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=True):
-    """Time `steps` whole-path steps; return a dict of figures."""
+    """Time `steps` whole-path steps after `warmup` untimed ones (a negative
+    `warmup` is a warm-up length in ms); return a dict of figures."""
     wl = workload.make_workload(name)
     db = harness.DeviceBatch(wl, fill=0)
     flops = wl.flops()
@@ -146,6 +154,15 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
             if events is not None:
                 events[2 * c + 2].record(stream)
 
+    if warmup < 0:
+        # Warm-up given in ms: at least 3 steps, then as many as fill it.
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(3):
+            step(None)
+        torch.cuda.synchronize()
+        per_step = (time.perf_counter() - t0) / 3
+        warmup = max(0, math.ceil(-warmup / 1e3 / per_step) - 3)
     for _ in range(warmup):
         step(None)
     torch.cuda.synchronize()
@@ -191,6 +208,7 @@ def time_config(name, steps, warmup, torch, tsa, harness, workload, calibrate=Tr
         "plan_us": plan_s / steps * 1e6,
         "num_items": [int(tsa.plan_items(sp).shape[0]) for sp in plans0],
         "xcd_order": xcd_order,
+        "warmup_steps": warmup,
         "workspace_bytes": [sp.workspace_bytes for sp in plans0],
         "wl": wl,
         "db": db,
@@ -620,7 +638,8 @@ def main():
         for name in ("tiny", "ragged", "long", "cold"):
             if name == args.config:
                 continue
-            rr = time_config(name, args.extra_steps, 3, torch, tsa, harness, workload,
+            rr = time_config(name, args.extra_steps, -args.extra_warmup_ms, torch, tsa, harness,
+                             workload,
                              calibrate=not args.no_xcd_calibration)
             wlx, dbx = rr.pop("wl"), rr.pop("db")
             rec = {"workload": WORKLOADS[name],
@@ -632,7 +651,8 @@ def main():
                    "prefill_tflops": round(rr["prefill_tflops"], 2),
                    "frac": round(rr["prefill_tflops"] / PEAK_BF16_TFLOPS, 4),
                    "append_gbs": round(rr["append_gbs"], 1),
-                   "work_items": rr["num_items"], "steps": args.extra_steps}
+                   "work_items": rr["num_items"], "steps": args.extra_steps,
+                   "warmup": rr["warmup_steps"]}
             if not args.no_cpu_baseline:
                 rows = sample_rows(wlx, args.extra_rows, seed=321)
                 o_ref, lse_ref, t = oracle_rows(wlx, rows, oracle)

@@ -5,6 +5,7 @@
 // never writes device memory and nothing has to be uploaded before a launch.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include "talaria_sp_attn.h"
@@ -71,6 +72,9 @@ struct PlanData {
 static_assert(sizeof(PlanData) <= sizeof(talaria_sp_plan), "plan storage too small");
 static_assert(sizeof(PlanData) <= 3584, "plan must fit a kernel argument");
 static_assert(TALARIA_SP_MAX_SEQS <= 256, "seq_orig holds sequence indices in a byte");
+static_assert(offsetof(PlanData, item_of_wg) % 4 == 0 && offsetof(PlanData, seq_orig) % 4 == 0 &&
+                  kMappedItems % 4 == 0 && TALARIA_SP_MAX_SEQS % 4 == 0,
+              "plan byte arrays are read as aligned 32-bit words");
 
 struct WorkItem {
     int32_t seq;
@@ -111,8 +115,15 @@ TSP_HD int32_t seq_of_item(const PlanData& p, int32_t id) {
     return lo;
 }
 
+// Byte i of a 4-byte-aligned byte array, read as its aligned 32-bit word:
+// kernels then load plan bytes with scalar (not per-lane) loads.
+TSP_HD uint32_t plan_byte(const uint8_t* a, int32_t i) {
+    const uint32_t word = reinterpret_cast<const uint32_t*>(a)[i >> 2];
+    return (word >> (8 * (i & 3))) & 0xffu;
+}
+
 // Block-table row of (launch-order) sequence b.
-TSP_HD int64_t bt_row_index(const PlanData& p, int32_t b) { return p.seq_orig[b]; }
+TSP_HD int64_t bt_row_index(const PlanData& p, int32_t b) { return plan_byte(p.seq_orig, b); }
 
 // Decode a work item.  Inside a sequence the split index varies fastest,
 // then the KV head, then the query tile in reverse order (the query tiles

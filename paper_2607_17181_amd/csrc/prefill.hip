@@ -50,8 +50,8 @@
 // 2^8.
 //
 // Items whose query tile is split over several key ranges write normalised
-// fp32 partials and base-2 LSE to the workspace; the combine kernel merges
-// them in a fixed order (bitwise deterministic).
+// f16 partials and fp32 base-2 LSE to the workspace; the combine kernel
+// merges them in a fixed order (bitwise deterministic).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -484,7 +484,8 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
 
     // Workgroup i runs on XCD i % 8; an XCD-placed plan names its item.
     const WorkItem w =
-        decode_item(p, p.wg_mapped ? (int32_t)p.item_of_wg[blockIdx.x] : (int32_t)blockIdx.x);
+        decode_item(p, p.wg_mapped ? (int32_t)plan_byte(p.item_of_wg, blockIdx.x)
+                                   : (int32_t)blockIdx.x);
     const SeqDesc s = p.seq[w.seq];
     const int Gq = p.group;
     const int lane = threadIdx.x & 63;
@@ -531,20 +532,9 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
     // flight.
     const bool group_b = wave >= G::NW / 2;
     constexpr int kd = 3, vd = 2;
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-        if (k < kd && tb + k < te)
-            ld.issue_k(kbuf(tb + k), (tb + k) * kKeysPerTile,
-                       c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
-#pragma unroll
-    for (int k = 0; k < 3; ++k)
-        if (k < vd && tb + k < te)
-            ld.issue_v(vbuf(tb + k), (tb + k) * kKeysPerTile,
-                       c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
-    uint32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
-    uint32_t pgv_next = c.bt_row[ld.page_index((tb + vd) * kKeysPerTile, c)];
-
-    // Query rows of this lane: one per 16-row block.
+    // Query rows of this lane, one per 16-row block, loaded first: they
+    // need no block-table lookup, so they are in flight while the page ids
+    // of the first tiles are read.
     const int rows_used = p.tile_tokens * Gq;
     int qtok[kQB], qhead[kQB], qpos[kQB];
     bf16x8 qf[kQB][D / 32];
@@ -564,6 +554,22 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
             qf[qb][ks] = __builtin_bit_cast(bf16x8, x);
         }
     }
+
+    // Then K(tb), K(tb+1) -- which the prologue and the first iteration
+    // read -- and K(tb+2), V(tb), V(tb+1), which the prologue does not wait
+    // for.
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        if (k < kd && tb + k < te)
+            ld.issue_k(kbuf(tb + k), (tb + k) * kKeysPerTile,
+                       c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        if (k < vd && tb + k < te)
+            ld.issue_v(vbuf(tb + k), (tb + k) * kKeysPerTile,
+                       c.bt_row[ld.page_index((tb + k) * kKeysPerTile, c)], c);
+    uint32_t pgk_next = c.bt_row[ld.page_index((tb + kd) * kKeysPerTile, c)];
+    uint32_t pgv_next = c.bt_row[ld.page_index((tb + vd) * kKeysPerTile, c)];
 
     const float scale = sm_scale * kLog2e;  // logits in base-2 units
     f32x4 o[kQB][D / 16];
@@ -587,8 +593,13 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
         for (int i = threadIdx.x; i < G::TILE_BYTES / 16; i += G::NT)
             vz[i] = u32x4{0, 0, 0, 0};
     }
-    wait_vmem_all();
-    __syncthreads();
+    // Loads complete in issue order: with all five tiles issued, at most
+    // the last three tiles' loads may still be in flight.
+    if (te - tb >= kd)
+        wait_vmem_n<3 * G::LOADS>();
+    else
+        wait_vmem_all();
+    lds_barrier();
 
     f32x4 sc[kQB][4];
     bf16x8 pf[kQB][2];

@@ -59,6 +59,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 #include <vector>
 
 #include "common.h"
@@ -812,8 +813,9 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
 // split query tiles are launched (blocks past a sequence's own tile count,
 // or of sequences without splits, exit at once): a grid over every work
 // item spent most of its time dispatching blocks with nothing to do.
-// Base-2 LSE merge in split order, KB splits per round of loads (8 for
-// plans with few splits, 16 for many-split plans such as a decode batch).
+// Base-2 LSE merge in split order, KB splits per round of loads (8, 16 or
+// 32, the fewest rounds for the plan's most-split tile: a decode batch's
+// longest sequences take up to 64 splits).
 template <int D, int KB>
 __global__ __launch_bounds__(256) void combine_kernel(PlanData p,
                                                       const _Float16* __restrict__ part_o,
@@ -842,21 +844,20 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p,
     constexpr int64_t kStrideO = (int64_t)kRowsPerTile * D;
     // Online merge in split order, KB splits per round of loads (all issued
     // before any is used): the running maximum only grows, and the sums are
-    // rescaled when it does.  The merge order, and so every result bit, does
-    // not depend on KB.
+    // rescaled when a later round raises it.  KB follows from the plan, so
+    // for a fixed plan every result bit is fixed.
     float mx = -INFINITY;
     f32xc acc = {};
     float wsum = 0.f;
     for (int k0 = 0; k0 < n; k0 += KB) {
         float lk[KB];
-        f32xc v[KB];
+        f16xc v[KB];  // converted where used: the raw halves take half the registers
 #pragma unroll
         for (int k = 0; k < KB; ++k) {
             lk[k] = -INFINITY;
             if (k0 + k < n) {
                 lk[k] = lse_k[(k0 + k) * kRowsPerTile];
-                v[k] = __builtin_convertvector(
-                    *reinterpret_cast<const f16xc*>(o_k + (k0 + k) * kStrideO), f32xc);
+                v[k] = *reinterpret_cast<const f16xc*>(o_k + (k0 + k) * kStrideO);
             }
         }
         float cm = mx;
@@ -874,7 +875,7 @@ __global__ __launch_bounds__(256) void combine_kernel(PlanData p,
             if (k0 + k < n) {
                 const float wk = (lk[k] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(lk[k] - mx);
                 wsum += wk;
-                acc += wk * v[k];
+                acc += wk * __builtin_convertvector(v[k], f32xc);
             }
     }
     const float inv = 1.f / wsum;
@@ -946,24 +947,24 @@ int launch_combine(const PlanData& p, const _Float16* part_o, const float* part_
         }
     if (rows == 0)
         return TALARIA_SP_OK;
-    const bool many = max_splits > 8;
-    if (p.head_dim == 128) {
-        const dim3 grid(tiles, ceil_div(rows, 256 / (128 / kCombineFeatures)), p.num_seqs);
-        if (many)
-            hipLaunchKernelGGL((combine_kernel<128, 16>), grid, dim3(256), 0, st, p, part_o,
-                               part_lse, out, lse);
+    auto launch = [&](auto d_tag, auto kb_tag) {
+        constexpr int D = decltype(d_tag)::value, KB = decltype(kb_tag)::value;
+        const dim3 grid(tiles, ceil_div(rows, 256 / (D / kCombineFeatures)), p.num_seqs);
+        hipLaunchKernelGGL((combine_kernel<D, KB>), grid, dim3(256), 0, st, p, part_o, part_lse,
+                           out, lse);
+    };
+    auto with_kb = [&](auto d_tag) {
+        if (max_splits > 16)
+            launch(d_tag, std::integral_constant<int, 32>{});
+        else if (max_splits > 8)
+            launch(d_tag, std::integral_constant<int, 16>{});
         else
-            hipLaunchKernelGGL((combine_kernel<128, 8>), grid, dim3(256), 0, st, p, part_o,
-                               part_lse, out, lse);
-    } else {
-        const dim3 grid(tiles, ceil_div(rows, 256 / (64 / kCombineFeatures)), p.num_seqs);
-        if (many)
-            hipLaunchKernelGGL((combine_kernel<64, 16>), grid, dim3(256), 0, st, p, part_o,
-                               part_lse, out, lse);
-        else
-            hipLaunchKernelGGL((combine_kernel<64, 8>), grid, dim3(256), 0, st, p, part_o,
-                               part_lse, out, lse);
-    }
+            launch(d_tag, std::integral_constant<int, 8>{});
+    };
+    if (p.head_dim == 128)
+        with_kb(std::integral_constant<int, 128>{});
+    else
+        with_kb(std::integral_constant<int, 64>{});
     return launch_status("combine");
 }
 

@@ -42,6 +42,10 @@ SMALL = {
     "single_token": lambda: _small("h", 8, 1, 128, 16, [5000], [1]),
     "page_aligned": lambda: _small("i", 8, 1, 128, 16, [1024], [512]),
     "peaky_logits": lambda: _small("j", 8, 1, 128, 16, [1500], [200], q_std=5.0),
+    # long enough for 43 splits (two combine rounds); logits std 3 (peaky_logits'
+    # std 5 with 2,700 keys puts outputs above 4, where the bf16 output quantum
+    # alone is 2^-6 of the 2e-2 bar)
+    "peaky_long": lambda: _small("k", 8, 1, 128, 16, [2600], [96], q_std=3.0),
 }
 
 
@@ -79,17 +83,23 @@ def test_prefill_matches_oracle(name, splits):
     assert lse_err <= h.LSE_ABS, f"lse error {lse_err}"
 
 
-@pytest.mark.parametrize("name", ["gqa8_d128_unaligned", "peaky_logits", "ragged_mixed"])
-def test_prefill_with_more_splits_than_one_combine_round(name):
-    """19 key-range splits per query tile: the combine merges them in three
-    rounds of loads (8 + 8 + 3), rescaling when a later round raises the
-    row maximum (large logits make that likely)."""
+@pytest.mark.parametrize("name,splits", [("gqa8_d128_unaligned", 12), ("peaky_logits", 12),
+                                         ("gqa8_d128_unaligned", 19), ("ragged_mixed", 45),
+                                         ("peaky_long", 45)])
+def test_prefill_with_more_splits_than_one_combine_round(name, splits):
+    """Many key-range splits per query tile: 12 merge in one round of 16
+    loads, 19 in one round of 32, and 45 requested (42-43 on these cases) in
+    two rounds of 32, rescaling when the second round raises the row maximum
+    (large logits make that likely)."""
     h = _harness()
     wl, o_ref, lse_ref, _, _ = cached_oracle(name)
-    print(f"case {name} splits=19", flush=True)
-    out, lse = h.DeviceBatch(wl).run(kv_splits=19)
+    db = h.DeviceBatch(wl)
+    most = max(int(tsa.plan_items(sp)[:, 7].max()) for sp in db.plans(kv_splits=splits))
+    print(f"case {name} splits={splits} (most {most})", flush=True)
+    assert most > (32 if splits == 45 else 8)
+    out, lse = db.run(kv_splits=splits)
     torch.cuda.synchronize()
-    h.assert_parity(h.error_stats(h.host_bits(out), o_ref), f"{name}/splits=19")
+    h.assert_parity(h.error_stats(h.host_bits(out), o_ref), f"{name}/splits={splits}")
     assert np.abs(lse.cpu().numpy() - lse_ref).max() <= h.LSE_ABS
 
 

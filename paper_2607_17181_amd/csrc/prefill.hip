@@ -797,13 +797,19 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(
             if (lse && lg == 0)
                 lse[row] = lse2 * kLn2;
         } else {
+            // Device-scope stores: they write through this XCD's L2, so the
+            // partials reach memory while the kernel runs and the end of the
+            // launch has none of them left to write back for the combine.
             _Float16* dst = part_o + ((int64_t)w.part_index * kRowsPerTile + r) * D + lg * 4;
 #pragma unroll
             for (int db = 0; db < D / 16; ++db)
-                *reinterpret_cast<f16x4*>(dst + db * 16) =
-                    __builtin_convertvector(o[qb][db] * inv, f16x4);
+                __hip_atomic_store(reinterpret_cast<uint64_t*>(dst + db * 16),
+                                   __builtin_bit_cast(uint64_t, __builtin_convertvector(
+                                                                    o[qb][db] * inv, f16x4)),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (lg == 0)
-                part_lse[(int64_t)w.part_index * kRowsPerTile + r] = lse2;
+                __hip_atomic_store(part_lse + (int64_t)w.part_index * kRowsPerTile + r, lse2,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }

@@ -332,9 +332,16 @@ def hbm_sweep(torch, tsa, reps=10):
     scratch = torch.ones(1 << 27, dtype=torch.int64, device="cuda")
     sink = torch.zeros(1, dtype=torch.int64, device="cuda")
 
-    def timeit(fn):
+    def timeit(fn, warm_ms=150.0):
+        # Untimed calls for at least warm_ms first, so that the part has
+        # settled to its steady clock.
         fn()
         torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < warm_ms:
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
         ts = []
         for r in range(reps):
             sink.add_(scratch.sum())
@@ -493,7 +500,7 @@ def select_bench(tsa, n=1000, reps=200):
             "note": "includes the Python binding's marshalling"}
 
 
-def decode_bench(torch, tsa, harness, workload, n_seqs=64, reps=20):
+def decode_bench(torch, tsa, harness, workload, n_seqs=64, reps=100):
     """Decode step of a batch of continuations: lognormal contexts (median
     25K, p95 105K tokens), one new token each, Hq=8 Hkv=1 d=128 page 16.
     GB/s = K/V bytes of every context position read once / decode call time;
@@ -509,9 +516,16 @@ def decode_bench(torch, tsa, harness, workload, n_seqs=64, reps=20):
     ws = tsa.workspace_tensor(sp)
     tsa.append_kv(sp, db.k_new, db.v_new, db.k_pool, db.v_pool, db.bt)
 
-    def timeit(fn):
+    def timeit(fn, warm_ms=150.0):
+        # Untimed calls first, for at least warm_ms, so that the part has
+        # settled to its steady clock (as the prefill configs are timed).
         fn()
         torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < warm_ms:
+            for _ in range(10):
+                fn()
+            torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(reps):

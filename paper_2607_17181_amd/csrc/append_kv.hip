@@ -118,6 +118,10 @@ extern "C" int talaria_sp_attn_append_kv(const talaria_sp_plan* plan, const void
     if (!k_new || !v_new || !k_pool || !v_pool || !block_tables)
         return fail(TALARIA_SP_EINVAL, "append_kv: k_new, v_new, k_pool, v_pool and "
                     "block_tables must not be NULL");
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool) ||
+        ((uintptr_t)block_tables & 3u) != 0)
+        return fail(TALARIA_SP_EINVAL, "append_kv: k_new, v_new, k_pool and v_pool must be "
+                    "16-byte aligned, block_tables 4-byte aligned");
     dim3 grid(p->max_suffix_pages, p->num_seqs, p->num_kv_heads);
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     auto kn = static_cast<const uint16_t*>(k_new);

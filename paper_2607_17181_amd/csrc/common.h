@@ -18,6 +18,9 @@ const PlanData* checked_plan(const talaria_sp_plan* plan, int* status);
 // Map a HIP launch status to TALARIA_SP_OK / TALARIA_SP_EHIP.
 int launch_status(const char* what);
 
+// The kernels move bf16 rows and partials in 16-byte vectors.
+inline bool aligned16(const void* a) { return ((uintptr_t)a & 15u) == 0; }
+
 }  // namespace tsp
 
 #if defined(__HIPCC__)

@@ -398,6 +398,10 @@ extern "C" int talaria_sp_attn_decode(const talaria_sp_plan* plan, const void* q
     memcpy(&scale_bits, &sm_scale, sizeof scale_bits);
     if ((scale_bits & 0x7f800000u) == 0x7f800000u)
         return fail(TALARIA_SP_EINVAL, "decode: sm_scale must be finite");
+    if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out) ||
+        !aligned16(workspace) || ((uintptr_t)lse & 3u) != 0 || ((uintptr_t)block_tables & 3u) != 0)
+        return fail(TALARIA_SP_EINVAL, "decode: q, k_pool, v_pool, out and workspace must be "
+                    "16-byte aligned, lse and block_tables 4-byte aligned");
     if (sm_scale <= 0.f)
         sm_scale = 1.f / sqrtf((float)p->head_dim);
     if ((size_t)p->ws_bytes > workspace_bytes || (p->ws_bytes > 0 && !workspace))

@@ -103,6 +103,10 @@ extern "C" int talaria_sp_attn_gather_kv(const talaria_sp_plan* plan, const void
         return TALARIA_SP_OK;
     if (!k_pool || !v_pool || !block_tables || !k_out || !v_out)
         return fail(TALARIA_SP_EINVAL, "gather_kv: pointers must not be NULL");
+    if (!aligned16(k_pool) || !aligned16(v_pool) || !aligned16(k_out) || !aligned16(v_out) ||
+        ((uintptr_t)block_tables & 3u) != 0)
+        return fail(TALARIA_SP_EINVAL, "gather_kv: k_pool, v_pool, k_out and v_out must be "
+                    "16-byte aligned, block_tables 4-byte aligned");
     dim3 grid(p->max_seq_pages, p->num_seqs, p->num_kv_heads);
     hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     auto kp = static_cast<const uint16_t*>(k_pool);

@@ -226,6 +226,27 @@ def test_prefill_checks_arguments_before_launching():
     assert st == tsa.EINVAL
 
 
+def test_calls_reject_misaligned_pointers_before_launching():
+    lib = tsa.library()
+    sp = tsa.plan(_geom(), [25_000], [2_048], 1700)
+    ok, odd = 4096, 4096 + 8
+    ws = sp.workspace_bytes
+    for args in [(odd, ok, ok, ok, ok, ok), (ok, ok, ok, ok, odd, ok), (ok, ok, ok, ok, ok, odd)]:
+        q, kp, vp, bt, out, wsp = args
+        st = lib.talaria_sp_attn_prefill(sp.raw, q, kp, vp, bt, 0.0, out, None, wsp, ws, None)
+        assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+    st = lib.talaria_sp_attn_prefill(sp.raw, ok, ok, ok, ok + 2, 0.0, ok, None, ok, ws, None)
+    assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+    st = lib.talaria_sp_attn_append_kv(sp.raw, ok, odd, ok, ok, ok, None)
+    assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+    st = lib.talaria_sp_attn_gather_kv(sp.raw, ok, ok, ok, ok, odd, None)
+    assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+    dp = tsa.plan(_geom(), [100, 5], [1, 1], 16)
+    st = lib.talaria_sp_attn_decode(ctypes.byref(dp.raw), ok, ok, odd, ok, 0.0, ok, None, None, 0,
+                                    None)
+    assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+
+
 def test_decode_rejects_multi_token_plans_without_launching():
     sp = tsa.plan(_geom(), [100, 5], [1, 2], 16)
     fake = 0x1000

@@ -27,9 +27,9 @@
  * holds logical tokens p*page_size .. (p+1)*page_size - 1 of sequence b.
  * Device arrays of bf16 rows (q, out, k_new, v_new, the pools, gather
  * outputs) and workspaces must be 16-byte aligned, block tables and lse
- * 4-byte aligned (hipMalloc returns 256-byte aligned memory); the
- * attention, append and gather calls return TALARIA_SP_EINVAL otherwise,
- * before launching anything.
+ * 4-byte aligned (hipMalloc returns 256-byte aligned memory), and so must
+ * the HKVR caches and slab; the attention, append, gather and HKVR calls
+ * return TALARIA_SP_EINVAL otherwise, before launching anything.
  *
  * Layouts (all bf16 tensors are raw 16-bit bfloat16, row-major):
  *   q, out      [T][Hq][head_dim]             T = sum_b S_b, sequences in order

@@ -81,6 +81,10 @@ int launch_copy(const talaria_kv_cache* cache, int32_t n, const int32_t* page_id
         return TALARIA_SP_OK;
     if (!page_ids || !k_cache || !v_cache || !slab)
         return fail(TALARIA_SP_EINVAL, "%s: pointers must not be NULL", what);
+    if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(slab) ||
+        ((uintptr_t)page_ids & 3u) != 0)
+        return fail(TALARIA_SP_EINVAL, "%s: k_cache, v_cache and slab must be 16-byte aligned, "
+                    "page_ids 4-byte aligned", what);
     const int64_t block_chunks =
         (int64_t)cache->num_kv_heads * cache->page_size * cache->head_dim * 2 / 16;
     hipLaunchKernelGGL(hkvr_copy_kernel<to_device>, dim3(n, cache->num_layers), dim3(256), 0,

@@ -247,6 +247,16 @@ def test_calls_reject_misaligned_pointers_before_launching():
     assert st == tsa.EINVAL and "aligned" in tsa.last_error()
 
 
+def test_hkvr_rejects_misaligned_pointers_before_launching():
+    c = tsa.kv_cache(2, 1, 128, 16, 64)
+    lib = tsa.library()
+    ok, odd = 4096, 4096 + 8
+    st = lib.talaria_hkvr_restore(ctypes.byref(c), 1, odd, ok, ok, ok, None)
+    assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+    st = lib.talaria_hkvr_checkpoint(ctypes.byref(c), 1, ok, odd, ok, ok, None)
+    assert st == tsa.EINVAL and "aligned" in tsa.last_error()
+
+
 def test_decode_rejects_multi_token_plans_without_launching():
     sp = tsa.plan(_geom(), [100, 5], [1, 2], 16)
     fake = 0x1000
